@@ -1,0 +1,139 @@
+/*
+ * libbpt — one Blockwise Parallel Transformer layer on AMD Instinct MI355X (gfx950).
+ *
+ * The layer is a pre-LayerNorm GPT block (the paper builds on the GPT
+ * architecture; Section 4, "Model Configuration"):
+ *
+ *     U  = LN1(X);   Q = U Wq,  K = U Wk,  V = U Wv         (Algorithm 1, "project")
+ *     O  = softmax(Q_h K_h^T / sqrt(dh) + mask) V_h, per head (eq. 1), computed
+ *          blockwise with running max / sum rescaling (Section 3, eq. 3)
+ *     Hd = X + O Wo
+ *     Y  = Hd + GELU(LN2(Hd) W1 + b1) W2 + b2                 (eq. 2, GELU for ReLU)
+ *
+ * and, per Algorithm 1, the FFN and both residuals are applied to each group of
+ * query blocks right after that group's attention, before the next group
+ * starts, so that no S x S score matrix and no S x F FFN intermediate is ever
+ * stored. The backward recomputes attention probabilities blockwise from the
+ * saved log-sum-exp and the FFN intermediate per query-block group.
+ *
+ * Conventions (all entry points):
+ *  - Every pointer argument of a compute call is a DEVICE pointer on the
+ *    current HIP device, owned by the caller. The library never allocates or
+ *    frees device memory; all scratch comes from the caller's workspace.
+ *  - Matrices are row-major; y = x @ W with W[D_in, D_out]. Head h owns
+ *    columns [h*dh, (h+1)*dh) of Wq, Wk, Wv and rows [h*dh, (h+1)*dh) of Wo.
+ *  - X, dY, Wq..W2 and the saved activations are in cfg->dtype; Y and dX in
+ *    cfg->out_dtype. LayerNorm gains/shifts and FFN biases are always fp32
+ *    vectors and may be NULL (gain 1, shift 0, no bias). Weight gradients are
+ *    fp32 and OVERWRITTEN; a NULL gradient pointer skips that output.
+ *  - Every pointer must be 16-byte aligned. Y must not alias X; dX must not
+ *    alias dY or X; outputs must not overlap inputs, saved or workspace.
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *    stream) and never synchronise. Arguments are validated before anything
+ *    is launched, so on any error status nothing has been written. Faults
+ *    inside kernels surface at the caller's next synchronisation.
+ *  - Supported: dh = D/H in {64, 128}; D and F multiples of 64; B, S >= 1;
+ *    1 <= Bq, Bkv <= S. Other shapes return BPT_ERR_UNSUPPORTED.
+ *  - bpt_last_error() returns a thread-local message for the last failure.
+ */
+#ifndef LIBBPT_H
+#define LIBBPT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BPT_OK = 0,
+  BPT_ERR_INVALID_ARG = 1,  /* NULL pointer, non-positive size, D % H != 0, Bq > S ... */
+  BPT_ERR_UNSUPPORTED = 2,  /* valid but not implemented (dh, D % 64, dtype)          */
+  BPT_ERR_WORKSPACE = 3,    /* workspace smaller than bpt_workspace_bytes()            */
+  BPT_ERR_HIP = 4           /* a kernel launch was rejected by the HIP runtime         */
+} bpt_status;
+
+typedef enum { BPT_F32 = 0, BPT_BF16 = 1 } bpt_dtype;
+
+typedef struct {
+  int64_t B, S, D, H, F;   /* batch, sequence length, model width, heads, FFN width        */
+  int64_t Bq, Bkv;         /* query / key-value block LENGTHS in tokens (Section 3). Need  */
+                           /* not divide S. Bq is the unit of FFN fusion; Bkv is the KV   */
+                           /* step of the method. Results depend on them only through     */
+                           /* rounding (the method is exact).                              */
+  int32_t causal;          /* 1: query q sees key k iff k <= q, within one sequence        */
+  int32_t dtype;           /* bpt_dtype of X, dY, weights and saved activations             */
+  int32_t out_dtype;       /* bpt_dtype of Y and dX                                         */
+  int32_t group_blocks;    /* query blocks per FFN group (rows of the [., F] intermediate   */
+                           /* live at once = group_blocks * Bq); 0 = automatic              */
+  float ln_eps;            /* LayerNorm epsilon (biased variance), e.g. 1e-5                */
+} bpt_config;
+
+typedef struct {           /* device pointers; see the conventions above                    */
+  const float *ln1_g, *ln1_b;              /* [D] fp32 or NULL                               */
+  const void *Wq, *Wk, *Wv, *Wo;           /* [D, D] in cfg->dtype                           */
+  const float *ln2_g, *ln2_b;              /* [D] fp32 or NULL                               */
+  const void *W1;                          /* [D, F] in cfg->dtype                           */
+  const float *b1;                         /* [F] fp32 or NULL                               */
+  const void *W2;                          /* [F, D] in cfg->dtype                           */
+  const float *b2;                         /* [D] fp32 or NULL                               */
+} bpt_params;
+
+typedef struct {           /* fp32 device pointers, overwritten; NULL = not wanted          */
+  float *dln1_g, *dln1_b, *dWq, *dWk, *dWv, *dWo, *dln2_g, *dln2_b, *dW1, *db1, *dW2, *db2;
+} bpt_grads;
+
+/* Byte offsets of the tensors the forward saves for the backward, inside the
+ * caller's `saved` buffer. E = element size of cfg->dtype; T = B*S tokens;
+ * Sp = S rounded up to a multiple of 64.
+ *   qk   [T, 2D] E   Q (unscaled) in columns [0, D), K in [D, 2D)
+ *   vt   [D, B*Sp] E V transposed: V[b, s, f] at row f, column b*Sp + s; pad columns are 0
+ *   o    [T, D] E    attention output (heads concatenated), before Wo
+ *   lse  [B, H, Sp] fp32  natural-log log-sum-exp of each query row's scores
+ *   h    [T, D] fp32 residual stream after attention, X + O Wo
+ *   mu1, rstd1, mu2, rstd2 [T] fp32  LayerNorm statistics                               */
+typedef struct {
+  size_t qk, vt, o, lse, h, mu1, rstd1, mu2, rstd2, total;
+} bpt_saved_layout;
+
+/* Host-only checks of a configuration; never touches a GPU. */
+bpt_status bpt_validate(const bpt_config* cfg);
+
+/* Rows of the [., F] FFN intermediate that are live at once (group_blocks * Bq,
+ * clipped to S). Returns -1 for an invalid configuration. Host-only. */
+int64_t bpt_group_rows(const bpt_config* cfg);
+
+/* Size of the `saved` buffer and the offsets inside it. O(B*S*D); no S*S or S*F
+ * term. Returns 0 / a non-OK status for an invalid configuration. Host-only. */
+size_t bpt_saved_bytes(const bpt_config* cfg);
+bpt_status bpt_saved_layout_of(const bpt_config* cfg, bpt_saved_layout* out);
+
+/* Workspace needed by bpt_layer_fwd (backward = 0) or bpt_layer_bwd (backward = 1):
+ * O(D^2 + D*F + B*S*D + group_rows*F). Returns 0 for an invalid configuration. Host-only. */
+size_t bpt_workspace_bytes(const bpt_config* cfg, int backward);
+
+/* Forward of one layer (Algorithm 1). X, Y: [B, S, D]. `saved` (bpt_saved_bytes
+ * bytes) receives the activations the backward needs. Y must not alias X. */
+bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params* params, void* Y,
+                         void* saved, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward of one layer given the forward's `saved` buffer and the upstream
+ * gradient dY [B, S, D]. Writes dX [B, S, D] (out_dtype) and every non-NULL
+ * gradient in `grads`. Attention probabilities are rebuilt blockwise from the
+ * saved log-sum-exp; the FFN intermediate is recomputed per query-block group. */
+bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params* params,
+                         const void* saved, const void* dY, void* dX, const bpt_grads* grads,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+const char* bpt_status_string(int status);
+const char* bpt_last_error(void);
+
+/* Human-readable description of the kernel tiling used for a configuration
+ * (internal MFMA / LDS tiles, FFN group rows). Host-only. Returns bytes written. */
+size_t bpt_describe(const bpt_config* cfg, char* buf, size_t buf_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LIBBPT_H */

@@ -1,0 +1,105 @@
+// Host-side launchers shared between libbpt's translation units (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bpt {
+
+enum Dt { F32 = 0, BF16 = 1 };
+
+// ---------------------------------------------------------------- GEMM
+// C[M, N] = A[M, K] * B[N, K]^T ("NT": both operands K-contiguous), fp32 accumulation,
+// optional batch (grid z) with element strides, followed by a fused epilogue.
+enum Epi {
+  EPI_STORE = 0,   // C = acc            (fp32 C may accumulate: C += acc)
+  EPI_RESID = 1,   // C = acc + R[m, n] (+ bias[n])
+  EPI_GELU = 2,    // z = acc (+ bias[n] or bias[m]); C = GELU(z); C2 = GELU'(z) if C2
+  EPI_MUL = 3,     // C = acc * R[m, n]  (R fp32)
+};
+
+struct GemmArgs {
+  const void* A = nullptr;
+  const void* B = nullptr;
+  void* C = nullptr;
+  const void* R = nullptr;     // residual (EPI_RESID) or multiplier (EPI_MUL)
+  const float* bias = nullptr;
+  float* C2 = nullptr;         // second output of EPI_GELU
+  int64_t M = 0, N = 0, K = 0;
+  int64_t Nstore = 0;          // columns [N, Nstore) of C (and C2) are written with 0
+  int64_t lda = 0, ldb = 0, ldc = 0, ldr = 0, ldc2 = 0;
+  int64_t sA = 0, sB = 0, sC = 0, sR = 0, sC2 = 0;   // batch strides in elements
+  int batch = 1;
+  int accumulate = 0;          // fp32 C only: C += acc
+  int bias_on_m = 0;           // EPI_GELU: bias indexed by row instead of column
+};
+
+// ab: element type of A and B. ct: type of C; rt: type of R.
+hipError_t gemm(Dt ab, Epi epi, Dt ct, Dt rt, const GemmArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+  // token-major tensors: token (b, s) is row b*S + s
+  const void* q = nullptr;  int64_t ld_q = 0;    // pointer already at head 0's first column
+  const void* k = nullptr;  int64_t ld_k = 0;
+  const void* v = nullptr;  int64_t ld_v = 0;    // token-major V (backward)
+  const void* dout = nullptr; int64_t ld_do = 0;
+  void* o = nullptr;        int64_t ld_o = 0;
+  // feature-major tensors: element (b, s, f) at row f, column b*Sp + s
+  const void* vt = nullptr; int64_t ld_vt = 0;
+  const void* qt = nullptr; int64_t ld_qt = 0;
+  const void* kt = nullptr; int64_t ld_kt = 0;
+  const void* dot = nullptr; int64_t ld_dot = 0;
+  void* dqt = nullptr; void* dkt = nullptr; void* dvt = nullptr; int64_t ld_dt = 0;
+  float* lse = nullptr;        // [B, H, Sp] natural log
+  const float* delta = nullptr;// [B, H, Sp]
+  int64_t S = 0, Sp = 0;
+  int B = 0, H = 0, dh = 0;
+  int causal = 0;
+  int64_t q_begin = 0, q_end = 0;  // forward: query rows [q_begin, q_end) of batch b_begin
+  int b_begin = 0, nb = 0;
+};
+
+hipError_t attn_fwd(Dt dt, const AttnArgs& a, hipStream_t s);
+hipError_t attn_bwd(Dt dt, const AttnArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- row-wise / layout kernels
+// LayerNorm over D per row. x: [rows, D] (ti); out [rows, D] (to).
+// mode 0: compute and write mu/rstd; mode 1: use the given mu/rstd.
+hipError_t layer_norm(Dt ti, Dt to, const void* x, int64_t ldx, const float* g, const float* b,
+                      void* out, int64_t ldo, float* mu, float* rstd, int64_t rows, int64_t D,
+                      float eps, int use_stats, hipStream_t s);
+
+// out = resid + LN^T(dout), per row; out2 (optional, type t2) gets the same values.
+hipError_t layer_norm_bwd(Dt ti, const void* x, const float* mu, const float* rstd, const float* g,
+                          const float* dout, Dt tr, const void* resid, Dt to, void* out,
+                          Dt t2, void* out2, int64_t rows, int64_t D, hipStream_t s);
+
+// dgamma[d] = sum_r dout[r,d] * xhat[r,d]; dbeta[d] = sum_r dout[r,d] (overwrite).
+// `partial` is workspace of layer_norm_param_grad_ws(D) floats.
+size_t layer_norm_param_grad_ws(int64_t D);
+hipError_t layer_norm_param_grad(Dt ti, const void* x, const float* mu, const float* rstd,
+                                 const float* dout, float* dgamma, float* dbeta, float* partial,
+                                 int64_t rows, int64_t D, hipStream_t s);
+
+// out[c, r] = in[r, c] for r < rows, 0 for rows <= r < rows_store; batched over z.
+hipError_t transpose(Dt t, const void* in, int64_t ld_in, int64_t s_in, void* out, int64_t ld_out,
+                     int64_t s_out, int64_t rows, int64_t cols, int64_t rows_store, int batch,
+                     hipStream_t s);
+
+// out[r, c] = in[r, c]
+hipError_t copy2d(Dt t, const void* in, int64_t ld_in, void* out, int64_t ld_out, int64_t rows,
+                  int64_t cols, hipStream_t s);
+
+// out[c] (+)= sum_r in[r, c]  (in: [rows, cols] of type t)
+hipError_t col_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols, float* out,
+                   int accumulate, float* partial, hipStream_t s);
+// out[r] (+)= sum_c in[r, c]
+hipError_t row_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols, float* out,
+                   int accumulate, hipStream_t s);
+
+// delta[b, h, s] = sum_d dO[b*S+s, h*dh+d] * O[b*S+s, h*dh+d]
+hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, float* delta, int B,
+                      int64_t S, int64_t Sp, int H, int dh, hipStream_t s);
+
+}  // namespace bpt

@@ -1,0 +1,504 @@
+// libbpt host side: argument validation, buffer layout and the launch sequence of
+// one Blockwise Parallel Transformer layer (Algorithm 1 of the paper) forward and
+// backward. Allocates nothing on the device; every launch goes to the caller's
+// stream and nothing synchronises.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+
+#include "../../include/libbpt.h"
+#include "internal.h"
+
+using namespace bpt;
+
+namespace {
+
+thread_local std::string g_err;
+
+bpt_status fail(bpt_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+constexpr int64_t kAlign = 256;
+constexpr int64_t kDefaultGroupRows = 8192;   // target rows of the [., F] FFN intermediate
+
+int64_t rup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+size_t esize(int32_t dt) { return dt == BPT_BF16 ? 2 : 4; }
+
+struct Dims {
+  int64_t B, S, D, H, F, dh, T, Sp, Tp, R, Rp;
+  size_t E;
+};
+
+Dims dims_of(const bpt_config& c) {
+  Dims d;
+  d.B = c.B; d.S = c.S; d.D = c.D; d.H = c.H; d.F = c.F;
+  d.dh = c.D / c.H;
+  d.T = c.B * c.S;
+  d.Sp = rup(c.S, 64);
+  d.Tp = c.B * d.Sp;
+  const int64_t g = c.group_blocks > 0 ? c.group_blocks
+                                      : std::max<int64_t>(1, (kDefaultGroupRows + c.Bq - 1) / c.Bq);
+  d.R = std::min<int64_t>(g * c.Bq, c.S);
+  d.Rp = rup(d.R, 64);
+  d.E = esize(c.dtype);
+  return d;
+}
+
+bpt_status check(const bpt_config* c) {
+  if (!c) return fail(BPT_ERR_INVALID_ARG, "config is NULL");
+  if (c->B < 1 || c->S < 1 || c->D < 1 || c->H < 1 || c->F < 1)
+    return fail(BPT_ERR_INVALID_ARG, "B, S, D, H, F must be >= 1 (got %lld %lld %lld %lld %lld)",
+                (long long)c->B, (long long)c->S, (long long)c->D, (long long)c->H, (long long)c->F);
+  if (c->D % c->H != 0)
+    return fail(BPT_ERR_INVALID_ARG, "D=%lld is not divisible by H=%lld", (long long)c->D, (long long)c->H);
+  if (c->Bq < 1 || c->Bq > c->S || c->Bkv < 1 || c->Bkv > c->S)
+    return fail(BPT_ERR_INVALID_ARG, "block lengths must satisfy 1 <= Bq, Bkv <= S (got %lld, %lld, S=%lld)",
+                (long long)c->Bq, (long long)c->Bkv, (long long)c->S);
+  if (c->causal != 0 && c->causal != 1) return fail(BPT_ERR_INVALID_ARG, "causal must be 0 or 1");
+  if ((c->dtype != BPT_F32 && c->dtype != BPT_BF16) || (c->out_dtype != BPT_F32 && c->out_dtype != BPT_BF16))
+    return fail(BPT_ERR_INVALID_ARG, "dtype / out_dtype must be BPT_F32 or BPT_BF16");
+  if (c->group_blocks < 0) return fail(BPT_ERR_INVALID_ARG, "group_blocks must be >= 0");
+  if (!(c->ln_eps > 0.0f)) return fail(BPT_ERR_INVALID_ARG, "ln_eps must be > 0");
+  const int64_t dh = c->D / c->H;
+  if (dh != 64 && dh != 128)
+    return fail(BPT_ERR_UNSUPPORTED, "head dim D/H=%lld unsupported (64 or 128)", (long long)dh);
+  if (c->D % 64 != 0 || c->F % 64 != 0)
+    return fail(BPT_ERR_UNSUPPORTED, "D and F must be multiples of 64 (got %lld, %lld)", (long long)c->D,
+                (long long)c->F);
+  // element indices are 64-bit everywhere; grid dimensions are 32-bit
+  if (c->B > 65535 || c->H > 65535) return fail(BPT_ERR_UNSUPPORTED, "B and H must be <= 65535");
+  if (c->B * rup(c->S, 64) > (int64_t)1 << 40) return fail(BPT_ERR_UNSUPPORTED, "B*S too large");
+  return BPT_OK;
+}
+
+// Bump allocator over a caller-provided region. With a zero base the returned
+// "pointers" are the byte offsets, which is how the sizes and layouts are computed.
+struct Bump {
+  uintptr_t base;
+  int64_t off = 0;
+  explicit Bump(void* b) : base((uintptr_t)b) {}
+  void* take(int64_t bytes) {
+    off = rup(off, kAlign);
+    void* p = (void*)(base + (uintptr_t)off);
+    off += bytes;
+    return p;
+  }
+};
+
+struct SavedPtrs {
+  void *qk, *vt, *o;
+  float *lse, *h, *mu1, *rstd1, *mu2, *rstd2;
+};
+
+SavedPtrs saved_layout(const Dims& d, void* base, int64_t* total) {
+  Bump bp(base);
+  SavedPtrs s;
+  s.qk = bp.take(d.T * 2 * d.D * d.E);
+  s.vt = bp.take(d.D * d.Tp * d.E);
+  s.o = bp.take(d.T * d.D * d.E);
+  s.lse = (float*)bp.take(d.B * d.H * d.Sp * 4);
+  s.h = (float*)bp.take(d.T * d.D * 4);
+  s.mu1 = (float*)bp.take(d.T * 4);
+  s.rstd1 = (float*)bp.take(d.T * 4);
+  s.mu2 = (float*)bp.take(d.T * 4);
+  s.rstd2 = (float*)bp.take(d.T * 4);
+  *total = rup(bp.off, kAlign);
+  return s;
+}
+
+struct FwdWs {
+  void *wqkT, *wvT, *woT, *w1T, *w2T, *u, *vg, *gg;
+};
+
+FwdWs fwd_ws(const Dims& d, void* base, int64_t* total) {
+  Bump bp(base);
+  FwdWs w;
+  w.wqkT = bp.take(2 * d.D * d.D * d.E);
+  w.wvT = bp.take(d.D * d.D * d.E);
+  w.woT = bp.take(d.D * d.D * d.E);
+  w.w1T = bp.take(d.F * d.D * d.E);
+  w.w2T = bp.take(d.D * d.F * d.E);
+  w.u = bp.take(d.T * d.D * d.E);
+  w.vg = bp.take(d.R * d.D * d.E);
+  w.gg = bp.take(d.R * d.F * d.E);
+  *total = rup(bp.off, kAlign);
+  return w;
+}
+
+struct BwdWs {
+  void *w1T, *wcat;
+  void *vg, *vgT, *gT, *dzT, *dz, *dyT;
+  float* gpT;
+  float *dv, *dh, *dU, *delta, *partial, *scratch;
+  void *dhe, *dhT, *oT, *dO, *dOT, *V, *qT, *kT, *dqkvT, *dqkv, *u, *uT;
+};
+
+BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
+  Bump bp(base);
+  BwdWs w;
+  w.w1T = bp.take(d.F * d.D * d.E);
+  w.wcat = bp.take(3 * d.D * d.D * d.E);
+  w.vg = bp.take(d.R * d.D * d.E);
+  w.vgT = bp.take(d.D * d.Rp * d.E);
+  w.gT = bp.take(d.F * d.Rp * d.E);
+  w.gpT = (float*)bp.take(d.F * d.Rp * 4);
+  w.dzT = bp.take(d.F * d.Rp * d.E);
+  w.dz = bp.take(d.R * d.F * d.E);
+  w.dyT = bp.take(d.D * d.Rp * d.E);
+  w.dv = (float*)bp.take(d.T * d.D * 4);
+  w.dh = (float*)bp.take(d.T * d.D * 4);
+  w.dhe = bp.take(d.T * d.D * d.E);
+  w.dhT = bp.take(d.D * d.Tp * d.E);
+  w.oT = bp.take(d.D * d.Tp * d.E);
+  w.dO = bp.take(d.T * d.D * d.E);
+  w.dOT = bp.take(d.D * d.Tp * d.E);
+  w.delta = (float*)bp.take(d.B * d.H * d.Sp * 4);
+  w.V = bp.take(d.T * d.D * d.E);
+  w.qT = bp.take(d.D * d.Tp * d.E);
+  w.kT = bp.take(d.D * d.Tp * d.E);
+  w.dqkvT = bp.take(3 * d.D * d.Tp * d.E);
+  w.dqkv = bp.take(d.T * 3 * d.D * d.E);
+  w.u = bp.take(d.T * d.D * d.E);
+  w.uT = bp.take(d.D * d.Tp * d.E);
+  w.dU = (float*)bp.take(d.T * d.D * 4);
+  w.partial = (float*)bp.take((int64_t)layer_norm_param_grad_ws(std::max(d.D, d.F)) * 4);
+  w.scratch = (float*)bp.take(2 * std::max(d.D, d.F) * 4);
+  *total = rup(bp.off, kAlign);
+  return w;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+#define HIPCHK(expr)                                                                   \
+  do {                                                                                 \
+    hipError_t _e = (expr);                                                            \
+    if (_e != hipSuccess) return fail(BPT_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(_e)); \
+  } while (0)
+
+char* off(const void* p, int64_t bytes) { return (char*)p + bytes; }
+
+}  // namespace
+
+extern "C" {
+
+bpt_status bpt_validate(const bpt_config* cfg) { return check(cfg); }
+
+int64_t bpt_group_rows(const bpt_config* cfg) {
+  if (check(cfg) != BPT_OK) return -1;
+  return dims_of(*cfg).R;
+}
+
+size_t bpt_saved_bytes(const bpt_config* cfg) {
+  if (check(cfg) != BPT_OK) return 0;
+  int64_t total;
+  saved_layout(dims_of(*cfg), nullptr, &total);
+  return (size_t)total;
+}
+
+bpt_status bpt_saved_layout_of(const bpt_config* cfg, bpt_saved_layout* out) {
+  bpt_status st = check(cfg);
+  if (st != BPT_OK) return st;
+  if (!out) return fail(BPT_ERR_INVALID_ARG, "out is NULL");
+  int64_t total;
+  SavedPtrs s = saved_layout(dims_of(*cfg), nullptr, &total);
+  // with a null base every pointer equals its byte offset
+  out->qk = (size_t)(uintptr_t)s.qk;
+  out->vt = (size_t)(uintptr_t)s.vt;
+  out->o = (size_t)(uintptr_t)s.o;
+  out->lse = (size_t)(uintptr_t)s.lse;
+  out->h = (size_t)(uintptr_t)s.h;
+  out->mu1 = (size_t)(uintptr_t)s.mu1;
+  out->rstd1 = (size_t)(uintptr_t)s.rstd1;
+  out->mu2 = (size_t)(uintptr_t)s.mu2;
+  out->rstd2 = (size_t)(uintptr_t)s.rstd2;
+  out->total = (size_t)total;
+  return BPT_OK;
+}
+
+size_t bpt_workspace_bytes(const bpt_config* cfg, int backward) {
+  if (check(cfg) != BPT_OK) return 0;
+  int64_t total;
+  const Dims d = dims_of(*cfg);
+  if (backward) bwd_ws(d, nullptr, &total);
+  else fwd_ws(d, nullptr, &total);
+  return (size_t)total;
+}
+
+const char* bpt_status_string(int st) {
+  switch (st) {
+    case BPT_OK: return "BPT_OK";
+    case BPT_ERR_INVALID_ARG: return "BPT_ERR_INVALID_ARG";
+    case BPT_ERR_UNSUPPORTED: return "BPT_ERR_UNSUPPORTED";
+    case BPT_ERR_WORKSPACE: return "BPT_ERR_WORKSPACE";
+    case BPT_ERR_HIP: return "BPT_ERR_HIP";
+  }
+  return "BPT_ERR_UNKNOWN";
+}
+
+const char* bpt_last_error(void) { return g_err.c_str(); }
+
+size_t bpt_describe(const bpt_config* cfg, char* buf, size_t n) {
+  if (!buf || n == 0) return 0;
+  if (check(cfg) != BPT_OK) {
+    buf[0] = 0;
+    return 0;
+  }
+  const Dims d = dims_of(*cfg);
+  const bool bf = cfg->dtype == BPT_BF16;
+  int w = snprintf(buf, n,
+                   "dtype=%s attention: q-tile=%d kv-step=%d (%s); backward dK/dV kv-tile=%d q-step=%d, "
+                   "dQ q-tile=%d kv-step=%d; gemm: %s; ffn group rows=%lld (%lld query blocks of %lld)",
+                   bf ? "bf16" : "f32", bf ? 128 : 64, bf ? 64 : 32,
+                   bf ? "MFMA 32x32x16 bf16, fp32 accumulate" : "fp32 VALU",
+                   bf ? 128 : 64, bf ? 64 : 16, bf ? 128 : 64, bf ? 64 : 16,
+                   bf ? "MFMA bf16 256x256 or 128x128 tiles, K-step 64" : "fp32 VALU 64x64 tiles",
+                   (long long)d.R, (long long)((d.R + cfg->Bq - 1) / cfg->Bq), (long long)cfg->Bq);
+  return w < 0 ? 0 : std::min((size_t)w, n - 1);
+}
+
+bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params* p, void* Y, void* saved,
+                         void* ws, size_t ws_bytes, void* stream) {
+  bpt_status st = check(cfg);
+  if (st != BPT_OK) return st;
+  if (!X || !p || !Y || !saved || !ws) return fail(BPT_ERR_INVALID_ARG, "NULL X, params, Y, saved or workspace");
+  if (!p->Wq || !p->Wk || !p->Wv || !p->Wo || !p->W1 || !p->W2)
+    return fail(BPT_ERR_INVALID_ARG, "NULL weight pointer");
+  if (X == Y) return fail(BPT_ERR_INVALID_ARG, "Y must not alias X");
+  const void* ptrs[] = {X, Y, saved, ws, p->Wq, p->Wk, p->Wv, p->Wo, p->W1, p->W2,
+                        p->ln1_g, p->ln1_b, p->ln2_g, p->ln2_b, p->b1, p->b2};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", q);
+  const Dims d = dims_of(*cfg);
+  int64_t need, stotal;
+  FwdWs w = fwd_ws(d, ws, &need);
+  if ((int64_t)ws_bytes < need)
+    return fail(BPT_ERR_WORKSPACE, "workspace %zu bytes < required %lld", ws_bytes, (long long)need);
+  SavedPtrs sv = saved_layout(d, saved, &stotal);
+  hipStream_t s = (hipStream_t)stream;
+  const Dt E = cfg->dtype == BPT_BF16 ? BF16 : F32;
+  const Dt OUT = cfg->out_dtype == BPT_BF16 ? BF16 : F32;
+  const int64_t D = d.D, F = d.F, T = d.T, E_ = (int64_t)d.E;
+
+  // weights into the K-contiguous layouts the NT GEMMs read
+  HIPCHK(transpose(E, p->Wq, D, 0, w.wqkT, D, 0, D, D, D, 1, s));
+  HIPCHK(transpose(E, p->Wk, D, 0, off(w.wqkT, D * D * E_), D, 0, D, D, D, 1, s));
+  HIPCHK(transpose(E, p->Wv, D, 0, w.wvT, D, 0, D, D, D, 1, s));
+  HIPCHK(transpose(E, p->Wo, D, 0, w.woT, D, 0, D, D, D, 1, s));
+  HIPCHK(transpose(E, p->W1, F, 0, w.w1T, D, 0, D, F, D, 1, s));
+  HIPCHK(transpose(E, p->W2, D, 0, w.w2T, F, 0, F, D, F, 1, s));
+
+  // U = LN1(X); [Q | K] = U [Wq | Wk]; V^T = Wv^T U^T  (Algorithm 1: project the input)
+  HIPCHK(layer_norm(E, E, X, D, p->ln1_g, p->ln1_b, w.u, D, sv.mu1, sv.rstd1, T, D, cfg->ln_eps, 0, s));
+  {
+    GemmArgs g;
+    g.A = w.u; g.lda = D; g.B = w.wqkT; g.ldb = D; g.C = sv.qk; g.ldc = 2 * D;
+    g.M = T; g.N = 2 * D; g.K = D;
+    HIPCHK(gemm(E, EPI_STORE, E, F32, g, s));
+  }
+  {
+    GemmArgs g;
+    g.A = w.wvT; g.lda = D; g.sA = 0;
+    g.B = w.u; g.ldb = D; g.sB = d.S * D;
+    g.C = sv.vt; g.ldc = d.Tp; g.sC = d.Sp;
+    g.M = D; g.N = d.S; g.Nstore = d.Sp; g.K = D; g.batch = (int)d.B;
+    HIPCHK(gemm(E, EPI_STORE, E, F32, g, s));
+  }
+
+  // Outer loop over groups of query blocks: attention for the group, then the
+  // output projection, LN2, FFN and both residuals for the same rows.
+  for (int64_t b = 0; b < d.B; ++b) {
+    for (int64_t s0 = 0; s0 < d.S; s0 += d.R) {
+      const int64_t r = std::min(d.R, d.S - s0);
+      const int64_t t0 = b * d.S + s0;
+      AttnArgs a;
+      a.q = sv.qk; a.ld_q = 2 * D;
+      a.k = off(sv.qk, D * E_); a.ld_k = 2 * D;
+      a.vt = sv.vt; a.ld_vt = d.Tp;
+      a.o = sv.o; a.ld_o = D;
+      a.lse = sv.lse;
+      a.S = d.S; a.Sp = d.Sp; a.B = (int)d.B; a.H = (int)d.H; a.dh = (int)d.dh; a.causal = cfg->causal;
+      a.q_begin = s0; a.q_end = s0 + r; a.b_begin = (int)b; a.nb = 1;
+      HIPCHK(attn_fwd(E, a, s));
+
+      GemmArgs go;     // h = X + O Wo
+      go.A = off(sv.o, t0 * D * E_); go.lda = D; go.B = w.woT; go.ldb = D;
+      go.C = sv.h + t0 * D; go.ldc = D; go.R = off(X, t0 * D * E_); go.ldr = D;
+      go.M = r; go.N = D; go.K = D;
+      HIPCHK(gemm(E, EPI_RESID, F32, E, go, s));
+
+      HIPCHK(layer_norm(F32, E, sv.h + t0 * D, D, p->ln2_g, p->ln2_b, w.vg, D, sv.mu2 + t0, sv.rstd2 + t0, r,
+                        D, cfg->ln_eps, 0, s));
+
+      GemmArgs g1;     // G = GELU(LN2(h) W1 + b1)
+      g1.A = w.vg; g1.lda = D; g1.B = w.w1T; g1.ldb = D; g1.C = w.gg; g1.ldc = F;
+      g1.bias = p->b1; g1.M = r; g1.N = F; g1.K = D;
+      HIPCHK(gemm(E, EPI_GELU, E, F32, g1, s));
+
+      GemmArgs g2;     // Y = h + G W2 + b2
+      g2.A = w.gg; g2.lda = F; g2.B = w.w2T; g2.ldb = F; g2.C = off(Y, t0 * D * esize(cfg->out_dtype));
+      g2.ldc = D; g2.R = sv.h + t0 * D; g2.ldr = D; g2.bias = p->b2; g2.M = r; g2.N = D; g2.K = F;
+      HIPCHK(gemm(E, EPI_RESID, OUT, F32, g2, s));
+    }
+  }
+  return BPT_OK;
+}
+
+bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params* p, const void* saved,
+                         const void* dY, void* dX, const bpt_grads* gr, void* ws, size_t ws_bytes,
+                         void* stream) {
+  bpt_status st = check(cfg);
+  if (st != BPT_OK) return st;
+  if (!X || !p || !saved || !dY || !dX || !ws)
+    return fail(BPT_ERR_INVALID_ARG, "NULL X, params, saved, dY, dX or workspace");
+  if (!p->Wq || !p->Wk || !p->Wv || !p->Wo || !p->W1 || !p->W2)
+    return fail(BPT_ERR_INVALID_ARG, "NULL weight pointer");
+  if (dX == dY || dX == X) return fail(BPT_ERR_INVALID_ARG, "dX must not alias dY or X");
+  bpt_grads G = {};
+  if (gr) G = *gr;
+  const void* ptrs[] = {X, saved, dY, dX, ws, p->Wq, p->Wk, p->Wv, p->Wo, p->W1, p->W2, p->ln1_g, p->ln1_b,
+                        p->ln2_g, p->ln2_b, p->b1, p->b2, G.dln1_g, G.dln1_b, G.dWq, G.dWk, G.dWv, G.dWo,
+                        G.dln2_g, G.dln2_b, G.dW1, G.db1, G.dW2, G.db2};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", q);
+  const Dims d = dims_of(*cfg);
+  int64_t need, stotal;
+  BwdWs w = bwd_ws(d, ws, &need);
+  if ((int64_t)ws_bytes < need)
+    return fail(BPT_ERR_WORKSPACE, "workspace %zu bytes < required %lld", ws_bytes, (long long)need);
+  SavedPtrs sv = saved_layout(d, (void*)saved, &stotal);
+  hipStream_t s = (hipStream_t)stream;
+  const Dt E = cfg->dtype == BPT_BF16 ? BF16 : F32;
+  const Dt OUT = cfg->out_dtype == BPT_BF16 ? BF16 : F32;
+  const int64_t D = d.D, F = d.F, T = d.T, Tp = d.Tp, Sp = d.Sp, S = d.S, E_ = (int64_t)d.E;
+  const int B = (int)d.B;
+
+  HIPCHK(transpose(E, p->W1, F, 0, w.w1T, D, 0, D, F, D, 1, s));
+  HIPCHK(copy2d(E, p->Wq, D, w.wcat, 3 * D, D, D, s));
+  HIPCHK(copy2d(E, p->Wk, D, off(w.wcat, D * E_), 3 * D, D, D, s));
+  HIPCHK(copy2d(E, p->Wv, D, off(w.wcat, 2 * D * E_), 3 * D, D, D, s));
+
+  // ---- FFN and LN2 backward, per group of query blocks, recomputing the FFN intermediate
+  bool first = true;
+  for (int64_t b = 0; b < d.B; ++b) {
+    for (int64_t s0 = 0; s0 < S; s0 += d.R) {
+      const int64_t r = std::min(d.R, S - s0), rp = rup(r, 64), t0 = b * S + s0;
+      const void* dYg = off(dY, t0 * D * E_);
+      HIPCHK(layer_norm(F32, E, sv.h + t0 * D, D, p->ln2_g, p->ln2_b, w.vg, D, sv.mu2 + t0, sv.rstd2 + t0, r,
+                        D, cfg->ln_eps, 1, s));
+      {   // Z^T = W1^T v^T: G^T = GELU(Z^T + b1), GELU'(Z^T)
+        GemmArgs g;
+        g.A = w.w1T; g.lda = D; g.B = w.vg; g.ldb = D; g.C = w.gT; g.ldc = d.Rp; g.C2 = w.gpT; g.ldc2 = d.Rp;
+        g.bias = p->b1; g.bias_on_m = 1; g.M = F; g.N = r; g.Nstore = rp; g.K = D;
+        HIPCHK(gemm(E, EPI_GELU, E, F32, g, s));
+      }
+      {   // dZ^T = (W2 dY^T) * GELU'(Z^T)
+        GemmArgs g;
+        g.A = p->W2; g.lda = D; g.B = dYg; g.ldb = D; g.C = w.dzT; g.ldc = d.Rp; g.R = w.gpT; g.ldr = d.Rp;
+        g.M = F; g.N = r; g.Nstore = rp; g.K = D;
+        HIPCHK(gemm(E, EPI_MUL, E, F32, g, s));
+      }
+      if (G.db1) HIPCHK(row_sum(E, w.dzT, d.Rp, F, r, G.db1, first ? 0 : 1, s));
+      if (G.dW2) {   // dW2 = G^T dY
+        HIPCHK(transpose(E, dYg, D, 0, w.dyT, d.Rp, 0, r, D, rp, 1, s));
+        GemmArgs g;
+        g.A = w.gT; g.lda = d.Rp; g.B = w.dyT; g.ldb = d.Rp; g.C = G.dW2; g.ldc = D;
+        g.M = F; g.N = D; g.K = rp; g.accumulate = first ? 0 : 1;
+        HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+      }
+      HIPCHK(transpose(E, w.dzT, d.Rp, 0, w.dz, F, 0, F, r, F, 1, s));
+      {   // dv = dZ W1^T
+        GemmArgs g;
+        g.A = w.dz; g.lda = F; g.B = p->W1; g.ldb = F; g.C = w.dv + t0 * D; g.ldc = D;
+        g.M = r; g.N = D; g.K = F;
+        HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+      }
+      if (G.dW1) {   // dW1 = v^T dZ
+        HIPCHK(transpose(E, w.vg, D, 0, w.vgT, d.Rp, 0, r, D, rp, 1, s));
+        GemmArgs g;
+        g.A = w.vgT; g.lda = d.Rp; g.B = w.dzT; g.ldb = d.Rp; g.C = G.dW1; g.ldc = F;
+        g.M = D; g.N = F; g.K = rp; g.accumulate = first ? 0 : 1;
+        HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+      }
+      first = false;
+    }
+  }
+  // dh = dY + LN2^T(dv)
+  HIPCHK(layer_norm_bwd(F32, sv.h, sv.mu2, sv.rstd2, p->ln2_g, w.dv, E, dY, F32, w.dh, E, w.dhe, T, D, s));
+  if (G.dln2_g || G.dln2_b)
+    HIPCHK(layer_norm_param_grad(F32, sv.h, sv.mu2, sv.rstd2, w.dv, G.dln2_g ? G.dln2_g : w.scratch,
+                                 G.dln2_b ? G.dln2_b : w.scratch + D, w.partial, T, D, s));
+  if (G.db2) HIPCHK(col_sum(E, dY, D, T, D, G.db2, 0, w.partial, s));
+
+  // ---- output projection backward: dO = dh Wo^T, dWo = O^T dh
+  {
+    GemmArgs g;
+    g.A = w.dhe; g.lda = D; g.B = p->Wo; g.ldb = D; g.C = w.dO; g.ldc = D; g.M = T; g.N = D; g.K = D;
+    HIPCHK(gemm(E, EPI_STORE, E, F32, g, s));
+  }
+  if (G.dWo) {
+    HIPCHK(transpose(E, sv.o, D, S * D, w.oT, Tp, Sp, S, D, Sp, B, s));
+    HIPCHK(transpose(E, w.dhe, D, S * D, w.dhT, Tp, Sp, S, D, Sp, B, s));
+    GemmArgs g;
+    g.A = w.oT; g.lda = Tp; g.B = w.dhT; g.ldb = Tp; g.C = G.dWo; g.ldc = D; g.M = D; g.N = D; g.K = Tp;
+    HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+  }
+
+  // ---- attention backward, probabilities rebuilt from the saved log-sum-exp
+  HIPCHK(attn_delta(E, w.dO, sv.o, D, w.delta, B, S, Sp, (int)d.H, (int)d.dh, s));
+  HIPCHK(transpose(E, sv.vt, Tp, Sp, w.V, D, S * D, D, S, D, B, s));
+  HIPCHK(transpose(E, sv.qk, 2 * D, S * 2 * D, w.qT, Tp, Sp, S, D, Sp, B, s));
+  HIPCHK(transpose(E, off(sv.qk, D * E_), 2 * D, S * 2 * D, w.kT, Tp, Sp, S, D, Sp, B, s));
+  HIPCHK(transpose(E, w.dO, D, S * D, w.dOT, Tp, Sp, S, D, Sp, B, s));
+  {
+    AttnArgs a;
+    a.q = sv.qk; a.ld_q = 2 * D;
+    a.k = off(sv.qk, D * E_); a.ld_k = 2 * D;
+    a.v = w.V; a.ld_v = D;
+    a.dout = w.dO; a.ld_do = D;
+    a.qt = w.qT; a.ld_qt = Tp;
+    a.kt = w.kT; a.ld_kt = Tp;
+    a.dot = w.dOT; a.ld_dot = Tp;
+    a.dqt = w.dqkvT; a.dkt = off(w.dqkvT, D * Tp * E_); a.dvt = off(w.dqkvT, 2 * D * Tp * E_); a.ld_dt = Tp;
+    a.lse = sv.lse; a.delta = w.delta;
+    a.S = S; a.Sp = Sp; a.B = B; a.H = (int)d.H; a.dh = (int)d.dh; a.causal = cfg->causal;
+    HIPCHK(attn_bwd(E, a, s));
+  }
+
+  // ---- QKV projection and LN1 backward
+  HIPCHK(transpose(E, w.dqkvT, Tp, Sp, w.dqkv, 3 * D, S * 3 * D, 3 * D, S, 3 * D, B, s));
+  if (G.dWq || G.dWk || G.dWv) {
+    HIPCHK(layer_norm(E, E, X, D, p->ln1_g, p->ln1_b, w.u, D, sv.mu1, sv.rstd1, T, D, cfg->ln_eps, 1, s));
+    HIPCHK(transpose(E, w.u, D, S * D, w.uT, Tp, Sp, S, D, Sp, B, s));
+    float* outs[3] = {G.dWq, G.dWk, G.dWv};
+    for (int i = 0; i < 3; ++i) {
+      if (!outs[i]) continue;
+      GemmArgs g;
+      g.A = w.uT; g.lda = Tp; g.B = off(w.dqkvT, i * D * Tp * E_); g.ldb = Tp; g.C = outs[i]; g.ldc = D;
+      g.M = D; g.N = D; g.K = Tp;
+      HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+    }
+  }
+  {
+    GemmArgs g;   // dU = [dQ dK dV] [Wq Wk Wv]^T
+    g.A = w.dqkv; g.lda = 3 * D; g.B = w.wcat; g.ldb = 3 * D; g.C = w.dU; g.ldc = D; g.M = T; g.N = D;
+    g.K = 3 * D;
+    HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+  }
+  HIPCHK(layer_norm_bwd(E, X, sv.mu1, sv.rstd1, p->ln1_g, w.dU, F32, w.dh, OUT, dX, OUT, nullptr, T, D, s));
+  if (G.dln1_g || G.dln1_b)
+    HIPCHK(layer_norm_param_grad(E, X, sv.mu1, sv.rstd1, w.dU, G.dln1_g ? G.dln1_g : w.scratch,
+                                 G.dln1_b ? G.dln1_b : w.scratch + D, w.partial, T, D, s));
+  return BPT_OK;
+}
+
+}  // extern "C"

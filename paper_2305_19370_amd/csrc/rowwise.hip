@@ -1,0 +1,332 @@
+// Row-wise and layout kernels of the BPT layer: LayerNorm forward / backward and
+// its parameter gradients, bias gradients (row / column sums), the softmax
+// backward's per-row Delta = rowsum(dO * O), transposes into the feature-major
+// layouts the MFMA kernels read, and a strided copy. All are HBM-bound; each
+// reads and writes every element once (LayerNorm re-reads its row from cache).
+#include "common.h"
+#include "internal.h"
+
+namespace bpt {
+
+template <typename T> struct Vec4;
+template <> struct Vec4<float> {
+  static BPT_DEV void load(const float* p, float v[4]) {
+    const f32x4 x = *(const f32x4*)p;
+    v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
+  }
+  static BPT_DEV void store(float* p, const float v[4]) { *(f32x4*)p = f32x4{v[0], v[1], v[2], v[3]}; }
+};
+template <> struct Vec4<bf16> {
+  static BPT_DEV void load(const bf16* p, float v[4]) {
+    const bf16x4 x = *(const bf16x4*)p;
+    v[0] = (float)x[0]; v[1] = (float)x[1]; v[2] = (float)x[2]; v[3] = (float)x[3];
+  }
+  static BPT_DEV void store(bf16* p, const float v[4]) {
+    bf16x4 x;
+    x[0] = (bf16)v[0]; x[1] = (bf16)v[1]; x[2] = (bf16)v[2]; x[3] = (bf16)v[3];
+    *(bf16x4*)p = x;
+  }
+};
+
+// ------------------------------------------------------------------ LayerNorm forward
+// One wave per row; each lane walks groups of 4 columns. Two-pass mean / variance.
+template <typename TI, typename TO>
+__global__ __launch_bounds__(256) void ln_fwd_kernel(const TI* x, int64_t ldx, const float* g,
+                                                     const float* bb, TO* out, int64_t ldo, float* mu,
+                                                     float* rstd, int64_t rows, int64_t D, float eps,
+                                                     int use_stats) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const TI* xr = x + row * ldx;
+  float mean, rs;
+  if (!use_stats) {
+    float s = 0.0f;
+    for (int64_t d = 4 * lane; d < D; d += 256) {
+      float v[4];
+      Vec4<TI>::load(xr + d, v);
+      s += (v[0] + v[1]) + (v[2] + v[3]);
+    }
+    mean = warp_sum(s) / (float)D;
+    float q = 0.0f;
+    for (int64_t d = 4 * lane; d < D; d += 256) {
+      float v[4];
+      Vec4<TI>::load(xr + d, v);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) q = fmaf(v[e] - mean, v[e] - mean, q);
+    }
+    const float var = warp_sum(q) / (float)D;
+    rs = 1.0f / sqrtf(var + eps);
+    if (lane == 0) {
+      mu[row] = mean;
+      rstd[row] = rs;
+    }
+  } else {
+    mean = mu[row];
+    rs = rstd[row];
+  }
+  TO* orow = out + row * ldo;
+  for (int64_t d = 4 * lane; d < D; d += 256) {
+    float v[4];
+    Vec4<TI>::load(xr + d, v);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float y = (v[e] - mean) * rs;
+      if (g) y *= g[d + e];
+      if (bb) y += bb[d + e];
+      v[e] = y;
+    }
+    Vec4<TO>::store(orow + d, v);
+  }
+}
+
+// ------------------------------------------------------------------ LayerNorm backward
+// dz = rstd * (gd - mean(gd) - xhat * mean(gd * xhat)), gd = dout * gamma; out = resid + dz.
+template <typename TI, typename TR, typename TO, typename T2>
+__global__ __launch_bounds__(256) void ln_bwd_kernel(const TI* x, const float* mu, const float* rstd,
+                                                     const float* g, const float* dout, const TR* resid,
+                                                     TO* out, T2* out2, int64_t rows, int64_t D) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const TI* xr = x + row * D;
+  const float* dr = dout + row * D;
+  const float m = mu[row], rs = rstd[row];
+  float s1 = 0.0f, s2 = 0.0f;
+  for (int64_t d = 4 * lane; d < D; d += 256) {
+    float xv[4], dv[4];
+    Vec4<TI>::load(xr + d, xv);
+    Vec4<float>::load(dr + d, dv);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float gd = g ? dv[e] * g[d + e] : dv[e];
+      s1 += gd;
+      s2 = fmaf(gd, (xv[e] - m) * rs, s2);
+    }
+  }
+  s1 = warp_sum(s1) / (float)D;
+  s2 = warp_sum(s2) / (float)D;
+  for (int64_t d = 4 * lane; d < D; d += 256) {
+    float xv[4], dv[4], rv[4];
+    Vec4<TI>::load(xr + d, xv);
+    Vec4<float>::load(dr + d, dv);
+    Vec4<TR>::load(resid + row * D + d, rv);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float gd = g ? dv[e] * g[d + e] : dv[e];
+      const float xh = (xv[e] - m) * rs;
+      rv[e] += rs * (gd - s1 - xh * s2);
+    }
+    Vec4<TO>::store(out + row * D + d, rv);
+    if (out2) Vec4<T2>::store(out2 + row * D + d, rv);
+  }
+}
+
+// ------------------------------------------------------------------ column / row sums
+static constexpr int kChunks = 128;
+
+template <typename TI>
+__global__ __launch_bounds__(256) void ln_param_partial_kernel(const TI* x, const float* mu,
+                                                               const float* rstd, const float* dout,
+                                                               float* partial, int64_t rows, int64_t D) {
+  const int64_t d = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (d >= D) return;
+  const int64_t per = (rows + kChunks - 1) / kChunks;
+  const int64_t r0 = blockIdx.y * per, r1 = r0 + per < rows ? r0 + per : rows;
+  float sg = 0.0f, sb = 0.0f;
+  for (int64_t r = r0; r < r1; ++r) {
+    const float dv = dout[r * D + d];
+    sg = fmaf(dv, (to_f32<TI>(x[r * D + d]) - mu[r]) * rstd[r], sg);
+    sb += dv;
+  }
+  partial[(int64_t)blockIdx.y * D + d] = sg;
+  partial[(int64_t)(kChunks + blockIdx.y) * D + d] = sb;
+}
+
+__global__ __launch_bounds__(256) void chunk_reduce_kernel(const float* partial, float* out0,
+                                                           float* out1, int64_t D, int accumulate) {
+  const int64_t d = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (d >= D) return;
+  float s0 = 0.0f, s1 = 0.0f;
+  for (int c = 0; c < kChunks; ++c) {
+    s0 += partial[(int64_t)c * D + d];
+    if (out1) s1 += partial[(int64_t)(kChunks + c) * D + d];
+  }
+  if (out0) out0[d] = accumulate ? out0[d] + s0 : s0;
+  if (out1) out1[d] = accumulate ? out1[d] + s1 : s1;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void col_partial_kernel(const T* in, int64_t ld, int64_t rows,
+                                                          int64_t cols, float* partial) {
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= cols) return;
+  const int64_t per = (rows + kChunks - 1) / kChunks;
+  const int64_t r0 = blockIdx.y * per, r1 = r0 + per < rows ? r0 + per : rows;
+  float s = 0.0f;
+  for (int64_t r = r0; r < r1; ++r) s += to_f32<T>(in[r * ld + c]);
+  partial[(int64_t)blockIdx.y * cols + c] = s;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void row_sum_kernel(const T* in, int64_t ld, int64_t rows, int64_t cols,
+                                                      float* out, int accumulate) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  float s = 0.0f;
+  for (int64_t c = lane; c < cols; c += 64) s += to_f32<T>(in[row * ld + c]);
+  s = warp_sum(s);
+  if (lane == 0) out[row] = accumulate ? out[row] + s : s;
+}
+
+// ------------------------------------------------------------------ softmax-backward Delta
+template <typename T>
+__global__ __launch_bounds__(256) void delta_kernel(const T* dO, const T* O, int64_t ld, float* delta,
+                                                    int B, int64_t S, int64_t Sp, int H, int dh) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;     // over B * H * Sp
+  if (i >= (int64_t)B * H * Sp) return;
+  const int64_t s = i % Sp;
+  const int64_t bh = i / Sp;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  float acc = 0.0f;
+  if (s < S) {
+    const int64_t off = (b * S + s) * ld + (int64_t)h * dh;
+    for (int d = 0; d < dh; d += 4) {
+      float x[4], y[4];
+      Vec4<T>::load(dO + off + d, x);
+      Vec4<T>::load(O + off + d, y);
+      acc += (x[0] * y[0] + x[1] * y[1]) + (x[2] * y[2] + x[3] * y[3]);
+    }
+  }
+  delta[i] = acc;
+}
+
+// ------------------------------------------------------------------ transpose / copy
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* in, int64_t ld_in, int64_t s_in, T* out,
+                                                        int64_t ld_out, int64_t s_out, int64_t rows,
+                                                        int64_t cols, int64_t rows_store) {
+  __shared__ T tile[64][65];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  in += (int64_t)blockIdx.z * s_in;
+  out += (int64_t)blockIdx.z * s_out;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int64_t r = r0 + ty + 4 * i, c = c0 + tx;
+    tile[ty + 4 * i][tx] = (r < rows && c < cols) ? in[r * ld_in + c] : from_f32<T>(0.0f);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int64_t c = c0 + ty + 4 * i, r = r0 + tx;
+    if (c < cols && r < rows_store) out[c * ld_out + r] = tile[tx][ty + 4 * i];
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void copy2d_kernel(const T* in, int64_t ld_in, T* out, int64_t ld_out,
+                                                     int64_t rows, int64_t cols) {
+  const int64_t r = blockIdx.y;
+  for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < cols; c += (int64_t)gridDim.x * 256)
+    out[r * ld_out + c] = in[r * ld_in + c];
+}
+
+// ------------------------------------------------------------------ host launchers
+#define BPT_T(dt, T, ...) \
+  do {                   \
+    if ((dt) == F32) {   \
+      using T = float;   \
+      __VA_ARGS__;       \
+    } else {             \
+      using T = bf16;    \
+      __VA_ARGS__;       \
+    }                    \
+  } while (0)
+
+hipError_t layer_norm(Dt ti, Dt to, const void* x, int64_t ldx, const float* g, const float* b, void* out,
+                      int64_t ldo, float* mu, float* rstd, int64_t rows, int64_t D, float eps,
+                      int use_stats, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((rows + 3) / 4));
+  BPT_T(ti, TI, BPT_T(to, TO,
+        hipLaunchKernelGGL((ln_fwd_kernel<TI, TO>), grid, dim3(256), 0, s, (const TI*)x, ldx, g, b,
+                           (TO*)out, ldo, mu, rstd, rows, D, eps, use_stats)));
+  return hipGetLastError();
+}
+
+hipError_t layer_norm_bwd(Dt ti, const void* x, const float* mu, const float* rstd, const float* g,
+                          const float* dout, Dt tr, const void* resid, Dt to, void* out, Dt t2,
+                          void* out2, int64_t rows, int64_t D, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((rows + 3) / 4));
+  BPT_T(ti, TI, BPT_T(tr, TR, BPT_T(to, TO, BPT_T(t2, T2,
+        hipLaunchKernelGGL((ln_bwd_kernel<TI, TR, TO, T2>), grid, dim3(256), 0, s, (const TI*)x, mu,
+                           rstd, g, dout, (const TR*)resid, (TO*)out, (T2*)out2, rows, D)))));
+  return hipGetLastError();
+}
+
+size_t layer_norm_param_grad_ws(int64_t D) { return (size_t)2 * kChunks * (size_t)D; }
+
+hipError_t layer_norm_param_grad(Dt ti, const void* x, const float* mu, const float* rstd,
+                                 const float* dout, float* dgamma, float* dbeta, float* partial,
+                                 int64_t rows, int64_t D, hipStream_t s) {
+  const dim3 grid((unsigned)((D + 255) / 256), kChunks);
+  BPT_T(ti, TI, hipLaunchKernelGGL((ln_param_partial_kernel<TI>), grid, dim3(256), 0, s, (const TI*)x,
+                                   mu, rstd, dout, partial, rows, D));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)((D + 255) / 256)), dim3(256), 0, s, partial,
+                     dgamma, dbeta, D, 0);
+  return hipGetLastError();
+}
+
+hipError_t col_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols, float* out,
+                   int accumulate, float* partial, hipStream_t s) {
+  const dim3 grid((unsigned)((cols + 255) / 256), kChunks);
+  BPT_T(t, T, hipLaunchKernelGGL((col_partial_kernel<T>), grid, dim3(256), 0, s, (const T*)in, ld, rows,
+                                 cols, partial));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)((cols + 255) / 256)), dim3(256), 0, s, partial,
+                     out, (float*)nullptr, cols, accumulate);
+  return hipGetLastError();
+}
+
+hipError_t row_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols, float* out,
+                   int accumulate, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  BPT_T(t, T, hipLaunchKernelGGL((row_sum_kernel<T>), dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s,
+                                 (const T*)in, ld, rows, cols, out, accumulate));
+  return hipGetLastError();
+}
+
+hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, float* delta, int B, int64_t S,
+                      int64_t Sp, int H, int dh, hipStream_t s) {
+  const int64_t n = (int64_t)B * H * Sp;
+  BPT_T(t, T, hipLaunchKernelGGL((delta_kernel<T>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                                 (const T*)dout, (const T*)o, ld, delta, B, S, Sp, H, dh));
+  return hipGetLastError();
+}
+
+hipError_t transpose(Dt t, const void* in, int64_t ld_in, int64_t s_in, void* out, int64_t ld_out,
+                     int64_t s_out, int64_t rows, int64_t cols, int64_t rows_store, int batch,
+                     hipStream_t s) {
+  if (cols <= 0 || rows_store <= 0 || batch <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((cols + 63) / 64), (unsigned)((rows_store + 63) / 64), (unsigned)batch);
+  BPT_T(t, T, hipLaunchKernelGGL((transpose_kernel<T>), grid, dim3(256), 0, s, (const T*)in, ld_in, s_in,
+                                 (T*)out, ld_out, s_out, rows, cols, rows_store));
+  return hipGetLastError();
+}
+
+hipError_t copy2d(Dt t, const void* in, int64_t ld_in, void* out, int64_t ld_out, int64_t rows,
+                  int64_t cols, hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  const unsigned gx = (unsigned)((cols + 255) / 256 < 64 ? (cols + 255) / 256 : 64);
+  BPT_T(t, T, hipLaunchKernelGGL((copy2d_kernel<T>), dim3(gx, (unsigned)rows), dim3(256), 0, s,
+                                 (const T*)in, ld_in, (T*)out, ld_out, rows, cols));
+  return hipGetLastError();
+}
+
+}  // namespace bpt

@@ -1,0 +1,157 @@
+"""GPU parity: libbpt (through the C ABI) against the float64 oracle on the same
+seeded inputs. Shapes span several tiles with ragged tails; both causal and
+non-causal; fp32 and bf16 paths; LayerNorm affine parameters and FFN biases on.
+
+Gates (written in each test):
+  fp32: normwise max|diff| <= 1e-4 * max|ref| and elementwise relative error
+        <= 1e-4 wherever |ref| >= 1e-2 * rms(ref);
+  bf16: e_max = max|diff| / rms(ref) <= 2e-2 and e_mean = mean|diff| / rms(ref)
+        <= 2e-3 for outputs, attention intermediates and dX; weight gradients
+        (sums over every token of products of bf16-rounded operands) are held to
+        e_max <= 4e-2, e_mean <= 4e-3.
+"""
+import numpy as np
+import pytest
+import torch
+
+from bpt_inputs import WORKLOADS, make_inputs, small_workload
+from gpu_util import GRAD_NAMES, fp32_ok, run_gpu, run_oracle, say, stats, table
+
+pytestmark = pytest.mark.gpu
+
+BF16_OUT = dict(e_max=2e-2, e_mean=2e-3)
+BF16_WGRAD = dict(e_max=4e-2, e_mean=4e-3)
+
+
+def compare_all(w, inp, gpu, Yr, g, tol_kind, label):
+    rows, bad = [], []
+    names = ["Y", "dX"] + [n for n in GRAD_NAMES if n in gpu]
+    for n in names:
+        ref = Yr if n == "Y" else g[n]
+        if tol_kind == "fp32":
+            ok, s = fp32_ok(gpu[n].numpy(), ref)
+        else:
+            s = stats(gpu[n].numpy(), ref)
+            lim = BF16_OUT if n in ("Y", "dX", "dln1_g", "dln1_b", "dln2_g", "dln2_b", "db1", "db2") else BF16_WGRAD
+            ok = s["e_max"] <= lim["e_max"] and s["e_mean"] <= lim["e_mean"]
+        rows.append((n, s))
+        if not ok:
+            bad.append(n)
+    say(f"\n[{label}]\n" + table(rows))
+    assert not bad, f"{label}: out of tolerance: {bad}"
+
+
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("H", [4, 2])          # head dim 64 and 128
+def test_fp32_small_ragged(causal, H):
+    w = small_workload("f32", B=2, S=250, D=256, H=H, F=512, causal=causal, Bq=64, Bkv=64)
+    inp = make_inputs(w, seed=1, affine=True, biases=True)
+    say(f"case fp32 small {w.name}")
+    gpu = run_gpu(w, inp, group_blocks=2)
+    Yr, _, g = run_oracle(w, inp)
+    compare_all(w, inp, gpu, Yr, g, "fp32", w.name)
+
+
+def test_fp32_workload_s512():
+    w = WORKLOADS["fp32_s512_d256"]
+    inp = make_inputs(w, seed=0)
+    say(f"case {w.name}")
+    gpu = run_gpu(w, inp)
+    Yr, _, g = run_oracle(w, inp)
+    compare_all(w, inp, gpu, Yr, g, "fp32", w.name)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("S,H", [(250, 2), (700, 4)])
+def test_bf16_small_ragged(causal, S, H):
+    w = small_workload("bf16", B=2, S=S, D=256, H=H, F=512, causal=causal, Bq=128, Bkv=128)
+    inp = make_inputs(w, seed=2, affine=True, biases=True)
+    say(f"case bf16 small {w.name}")
+    gpu = run_gpu(w, inp, group_blocks=2)
+    Yr, _, g = run_oracle(w, inp)
+    compare_all(w, inp, gpu, Yr, g, "bf16", w.name)
+
+
+def test_bf16_saved_intermediates():
+    """Kernel-level parity on what the forward saves: Q, K, V^T (projection GEMMs),
+    O and log-sum-exp (attention), h (output projection + residual), LN statistics."""
+    w = small_workload("bf16", B=2, S=333, D=512, H=4, F=1024, causal=True, Bq=100, Bkv=100)
+    inp = make_inputs(w, seed=3, affine=True, biases=True)
+    say(f"case saved {w.name}")
+    gpu = run_gpu(w, inp, backward=False, saved_views=True, group_blocks=1)
+    Yr, c, _ = run_oracle(w, inp, backward=False)
+    sv = gpu["saved"]
+    B, S, D, H = w.B, w.S, w.D, w.H
+    Sp = (S + 63) // 64 * 64
+    vt = sv["vt"].view(D, B, Sp)
+    checks = {
+        "Q": (sv["qk"][:, :D].reshape(B, S, D), c["Q"]),
+        "K": (sv["qk"][:, D:].reshape(B, S, D), c["K"]),
+        "V": (vt[:, :, :S].permute(1, 2, 0), c["V"]),
+        "O": (sv["o"].reshape(B, S, D), c["O"]),
+        "lse": (sv["lse"][:, :, :S], c["lse"]),
+        "h": (sv["h"].reshape(B, S, D), c["Hd"]),
+        "mu1": (sv["mu1"].reshape(B, S), c["X"].mean(-1)),
+        "rstd1": (sv["rstd1"].reshape(B, S), c["rstd1"][..., 0]),
+        "rstd2": (sv["rstd2"].reshape(B, S), c["rstd2"][..., 0]),
+        "Y": (gpu["Y"], Yr),
+    }
+    rows, bad = [], []
+    for n, (got, ref) in checks.items():
+        s = stats(got.numpy(), ref)
+        rows.append((n, s))
+        if not (s["e_max"] <= 2e-2 and s["e_mean"] <= 2e-3):
+            bad.append(n)
+    assert torch.all(vt[:, :, S:] == 0), "padding columns of V^T must be zero"
+    say("\n" + table(rows))
+    assert not bad, bad
+
+
+@pytest.mark.parametrize("Bq,Bkv,groups", [(128, 128, 1), (64, 32, 3), (333, 333, 1), (1000, 7, 1)])
+def test_bf16_block_sizes(Bq, Bkv, groups):
+    """Bq / Bkv / FFN grouping change the result only through rounding."""
+    w = small_workload("bf16", B=1, S=1000, D=256, H=2, F=512, causal=True, Bq=Bq, Bkv=Bkv)
+    inp = make_inputs(w, seed=4)
+    say(f"case blocks Bq={Bq} Bkv={Bkv} groups={groups}")
+    gpu = run_gpu(w, inp, group_blocks=groups)
+    Yr, _, g = run_oracle(w, inp)
+    compare_all(w, inp, gpu, Yr, g, "bf16", f"Bq={Bq},Bkv={Bkv},g={groups}")
+
+
+def test_bf16_output_is_rounded_fp32_output():
+    """A bf16 Y / dX is the fp32 result rounded to nearest even (same kernels, other store)."""
+    w = small_workload("bf16", B=2, S=300, D=256, H=2, F=512, causal=True)
+    inp = make_inputs(w, seed=5)
+    a = run_gpu(w, inp, out_dtype="f32")
+    b = run_gpu(w, inp, out_dtype="bf16")
+    for n in ("Y", "dX"):
+        assert torch.equal(a[n].to(torch.bfloat16).float(), b[n]), n
+    for n in ("dWq", "dW1", "dW2"):
+        assert torch.equal(a[n], b[n]), n
+
+
+def test_causality_and_determinism():
+    w = small_workload("bf16", B=1, S=512, D=256, H=2, F=512, causal=True)
+    inp = make_inputs(w, seed=6)
+    a = run_gpu(w, inp, backward=False)
+    a2 = run_gpu(w, inp, backward=False)
+    assert torch.equal(a["Y"], a2["Y"]), "forward is not bitwise repeatable"
+    t = 300
+    inp2 = dict(inp)
+    X2 = inp["X"].clone()
+    X2[:, t:] = torch.randn(X2[:, t:].shape, generator=torch.Generator().manual_seed(9)).to(X2.dtype)
+    inp2["X"] = X2
+    b = run_gpu(w, inp2, backward=False)
+    assert torch.equal(a["Y"][:, :t], b["Y"][:, :t]), "future tokens changed past outputs"
+    assert not torch.equal(a["Y"][:, t:], b["Y"][:, t:])
+
+
+def test_bf16_workload_1b_s4096():
+    """The full 1B-shaped workload (B=2, S=4096, D=2048, H=16, F=8192), every output
+    and gradient against the unblocked fp64 oracle."""
+    w = WORKLOADS["bf16_1b_s4096"]
+    inp = make_inputs(w, seed=0)
+    say(f"case {w.name}")
+    gpu = run_gpu(w, inp)
+    Yr, _, g = run_oracle(w, inp)
+    compare_all(w, inp, gpu, Yr, g, "bf16", w.name)
