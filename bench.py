@@ -1,0 +1,197 @@
+#!/usr/bin/env python3
+"""One-GPU benchmark of the Blockwise Parallel Transformer layer (libbpt).
+
+A step is one forward (training mode, saving activations) plus one backward of
+the layer on one batch of synthetic seeded input, all through libbpt's HIP
+kernels. Default workload: the 7B-shaped layer (B=1, S=32768, D=4096, H=32,
+dh=128, F=16384, causal, Bq=Bkv=1024, bf16 operands with fp32 accumulation).
+
+Prints ONE JSON line:
+  value       model TFLOP/s of fwd+bwd, with model FLOP = 3 x fwd and
+              fwd = 8 B S D^2 + 4 B S D F + 2 B D S (S+1)   (causal)
+  roofline    the launch class with the largest total time, its algorithmic
+              flops (or bytes) per unit time measured with HIP events around
+              each of its launches in the timed steps, against MI355X peak
+  cpu_baseline  the float64 CPU oracle on a bounded sample of the same layer
+              shape (shorter sequence), same FLOP convention
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def model_flops_fwd(B, S, D, F, causal=True):
+    attn = 2 * B * D * S * (S + 1) if causal else 4 * B * S * S * D
+    return 8 * B * S * D * D + 4 * B * S * D * F + attn
+
+
+def cpu_baseline(w, sample_S: int):
+    """Time the float64 oracle (untuned) on [B=1, S=sample_S] of the workload's layer shape."""
+    import numpy as np
+    import oracle
+    from bpt_inputs import make_inputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([int(i.get("num_threads", 0)) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    ws = w.with_(B=1, S=sample_S, Bq=min(w.Bq, sample_S), Bkv=min(w.Bkv, sample_S), name=w.name + "_sample")
+    inp = make_inputs(ws, seed=0)
+    p = oracle.params_from_inputs(inp)
+    X, dY = inp["X"].double().numpy(), inp["dY"].double().numpy()
+    t0 = time.perf_counter()
+    Y, cache = oracle.layer_fwd(X, p, ws.H, ws.causal)
+    g = oracle.layer_bwd(cache, p, dY)
+    dt = time.perf_counter() - t0
+    assert np.isfinite(Y).all() and np.isfinite(g["dX"]).all()
+    fl = 3 * model_flops_fwd(1, sample_S, ws.D, ws.F, ws.causal)
+    return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"fwd+bwd of one sequence of {sample_S} tokens of the same layer shape "
+                      f"(D={ws.D}, H={ws.H}, F={ws.F}, causal), float64 numpy, {dt:.1f} s",
+            "seconds": dt}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="bf16_7b_s32768")
+    ap.add_argument("--cpu-sample-s", type=int, default=4096)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
+              "sharding of the layer is a design, not part of this build", file=sys.stderr)
+        return 2
+
+    import torch
+    from bpt_inputs import WORKLOADS, make_inputs
+    from paper_2305_19370_amd import bpt
+
+    w = WORKLOADS[args.workload]
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    print(f"[bench] workload {w.name}: B={w.B} S={w.S} D={w.D} H={w.H} F={w.F} Bq={w.Bq} Bkv={w.Bkv} "
+          f"dtype={w.dtype}", file=sys.stderr, flush=True)
+    inp = make_inputs(w, seed=0)
+    d = {k: (v.to(dev) if v is not None else None) for k, v in inp.items()}
+    del inp
+    cfg = bpt.make_config(w.B, w.S, w.D, w.H, w.F, w.Bq, w.Bkv, w.causal, w.dtype, w.dtype)
+    layer = bpt.Layer(cfg)
+    wsf = torch.empty(bpt.workspace_bytes(cfg, False), dtype=torch.uint8, device=dev)
+    wsb = torch.empty(bpt.workspace_bytes(cfg, True), dtype=torch.uint8, device=dev)
+    out_dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    Y = torch.empty(w.B, w.S, w.D, dtype=out_dt, device=dev)
+    dX = torch.empty_like(Y)
+    saved = torch.empty(bpt.saved_bytes(cfg), dtype=torch.uint8, device=dev)
+    shapes = {"dWq": (w.D, w.D), "dWk": (w.D, w.D), "dWv": (w.D, w.D), "dWo": (w.D, w.D),
+              "dW1": (w.D, w.F), "dW2": (w.F, w.D)}
+    grads = {k: torch.empty(s, dtype=torch.float32, device=dev) for k, s in shapes.items()}
+
+    def step():
+        bpt.layer_fwd(cfg, d["X"], d, Y, saved, wsf)
+        bpt.layer_bwd(cfg, d["X"], d, saved, d["dY"], dX, grads, wsb)
+
+    def fwd():
+        bpt.layer_fwd(cfg, d["X"], d, Y, saved, wsf)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done", file=sys.stderr, flush=True)
+
+    # forward alone
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        fwd()
+    e1.record()
+    torch.cuda.synchronize()
+    fwd_ms = e0.elapsed_time(e1) / args.steps
+
+    # timed fwd+bwd steps, with per-launch events from the library's profiler
+    torch.cuda.reset_peak_memory_stats()
+    bpt.profile_enable(True)
+    torch.cuda.synchronize()
+    e0.record()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    bpt.profile_enable(False)
+    prof = bpt.profile_report()
+    ms = e0.elapsed_time(e1) / args.steps
+    peak_hbm = torch.cuda.max_memory_allocated()
+    ok = bool(torch.isfinite(Y.float()).all() and torch.isfinite(dX.float()).all())
+    print(f"[bench] {args.steps} steps: {ms:.2f} ms/step (wall {wall / args.steps * 1e3:.2f}), fwd {fwd_ms:.2f} ms, "
+          f"finite={ok}", file=sys.stderr, flush=True)
+
+    ffwd = model_flops_fwd(w.B, w.S, w.D, w.F, w.causal)
+    value = 3 * ffwd / (ms / 1e3) / 1e12
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
+
+    # roofline entry: the launch class with the largest total time
+    top = max(prof.items(), key=lambda kv: kv[1]["ms"])
+    name, rec = top
+    if rec["flops"] > 0:
+        achieved = rec["flops"] / (rec["ms"] / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak}
+    else:
+        achieved = rec["bytes"] / (rec["ms"] / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS}
+    roof.update({"kernel": name, "launches_per_step": rec["count"] / args.steps,
+                 "avg_launch_ms": rec["ms"] / rec["count"], "traffic": None})
+    breakdown = {k: {"ms_per_step": v["ms"] / args.steps,
+                     "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["flops"] > 0 and v["ms"] > 0 else None,
+                     "gbs": (v["bytes"] / (v["ms"] / 1e3) / 1e9) if v["ms"] > 0 else None}
+                 for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["ms"])}
+
+    out = {
+        "metric": "BPT layer fwd+bwd TFLOP/s (% bf16 MFMA peak), tokens/s, peak HBM vs seq len",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "S": w.S, "D": w.D, "H": w.H, "F": w.F, "Bq": w.Bq,
+                   "Bkv": w.Bkv, "causal": w.causal, "group_rows": bpt.group_rows(cfg)},
+        "pct_of_peak": round(100 * value / peak, 2),
+        "tokens_per_s": round(w.B * w.S / (ms / 1e3), 1),
+        "fwd_ms": round(fwd_ms, 3),
+        "fwd_tflops": round(ffwd / (fwd_ms / 1e3) / 1e12, 2),
+        "peak_hbm_gib": round(peak_hbm / 2 ** 30, 3),
+        "roofline": roof,
+        "kernels": breakdown,
+    }
+    if not args.no_cpu_baseline:
+        print(f"[bench] cpu baseline (oracle) on S={args.cpu_sample_s} ...", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_s)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    return 0 if ok else 1
+
+
+if __name__ == "__main__":
+    sys.exit(main())

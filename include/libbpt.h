@@ -133,6 +133,17 @@ const char* bpt_last_error(void);
  * (internal MFMA / LDS tiles, FFN group rows). Host-only. Returns bytes written. */
 size_t bpt_describe(const bpt_config* cfg, char* buf, size_t buf_bytes);
 
+/* Launch timing for tooling (benchmarks, roofline reports). bpt_profile_enable(1)
+ * clears the record and brackets every later launch of bpt_layer_fwd / bpt_layer_bwd
+ * with two HIP events on the launch stream, tagged with the call site's name and
+ * its algorithmic flops and HBM bytes; bpt_profile_enable(0) stops recording.
+ * After the caller has synchronised those streams, bpt_profile_report writes a
+ * JSON object {name: {count, ms, flops, bytes}} into buf (NUL-terminated,
+ * truncated to buf_bytes) and returns its full length. Process-wide; not meant to
+ * be toggled while another thread is launching. */
+bpt_status bpt_profile_enable(int on);
+size_t bpt_profile_report(char* buf, size_t buf_bytes);
+
 #ifdef __cplusplus
 }
 #endif

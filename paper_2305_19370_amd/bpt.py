@@ -48,7 +48,8 @@ class SavedLayout(ctypes.Structure):
 
 
 EXPORTS = ("bpt_validate", "bpt_group_rows", "bpt_saved_bytes", "bpt_saved_layout_of", "bpt_workspace_bytes",
-           "bpt_layer_fwd", "bpt_layer_bwd", "bpt_status_string", "bpt_last_error", "bpt_describe")
+           "bpt_layer_fwd", "bpt_layer_bwd", "bpt_status_string", "bpt_last_error", "bpt_describe",
+           "bpt_profile_enable", "bpt_profile_report")
 
 _lib = None
 
@@ -83,6 +84,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.bpt_last_error.restype = ctypes.c_char_p
     lib.bpt_describe.argtypes = [P(Config), ctypes.c_char_p, c_sz]
     lib.bpt_describe.restype = c_sz
+    lib.bpt_profile_enable.argtypes = [c_i32]
+    lib.bpt_profile_enable.restype = c_i32
+    lib.bpt_profile_report.argtypes = [ctypes.c_char_p, c_sz]
+    lib.bpt_profile_report.restype = c_sz
     _lib = lib
     return lib
 
@@ -132,6 +137,21 @@ def describe(cfg: Config) -> str:
     buf = ctypes.create_string_buffer(1024)
     load().bpt_describe(ctypes.byref(cfg), buf, 1024)
     return buf.value.decode()
+
+
+def profile_enable(on: bool) -> None:
+    _check(load().bpt_profile_enable(int(on)))
+
+
+def profile_report() -> Dict[str, Dict[str, float]]:
+    """Per call-site launch timings recorded since profile_enable(True); call after a
+    device synchronisation."""
+    import json
+    lib = load()
+    n = lib.bpt_profile_report(None, 0)
+    buf = ctypes.create_string_buffer(n + 1)
+    lib.bpt_profile_report(buf, n + 1)
+    return json.loads(buf.value.decode())
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:

@@ -765,31 +765,36 @@ static hipError_t fwd_launch(Dt dt, const AttnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// part 0: dK, dV (key-outer); part 1: dQ (query-outer).
 template <int DH>
-static hipError_t bwd_launch(Dt dt, const AttnArgs& a, hipStream_t s) {
+static hipError_t bwd_launch(Dt dt, int part, const AttnArgs& a, hipStream_t s) {
   if (a.S <= 0 || a.B <= 0) return hipSuccess;
   if (dt == BF16) {
-    auto kdkv = attn_bwd_dkdv_bf16_kernel<DH>;
-    auto kdq = attn_bwd_dq_bf16_kernel<DH>;
-    hipError_t e = set_lds(kdkv, DkvCfg<DH>::LDS);
-    if (e == hipSuccess) e = set_lds(kdq, DqCfg<DH>::LDS);
-    if (e != hipSuccess) return e;
     const unsigned tiles = (unsigned)((a.Sp + 127) / 128);
-    hipLaunchKernelGGL(kdkv, dim3(tiles, a.H, a.B), dim3(256), DkvCfg<DH>::LDS, s, a);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kdq, dim3(tiles, a.H, a.B), dim3(256), DqCfg<DH>::LDS, s, a);
+    if (part == 0) {
+      auto k = attn_bwd_dkdv_bf16_kernel<DH>;
+      hipError_t e = set_lds(k, DkvCfg<DH>::LDS);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(k, dim3(tiles, a.H, a.B), dim3(256), DkvCfg<DH>::LDS, s, a);
+    } else {
+      auto k = attn_bwd_dq_bf16_kernel<DH>;
+      hipError_t e = set_lds(k, DqCfg<DH>::LDS);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(k, dim3(tiles, a.H, a.B), dim3(256), DqCfg<DH>::LDS, s, a);
+    }
   } else {
-    const int lds_kv = (2 * DH * 65 + 2 * 16 * DH + 32) * 4;
-    const int lds_q = (2 * DH * 65 + 2 * 16 * DH) * 4;
-    hipError_t e = set_lds(attn_bwd_dkdv_f32_kernel<DH>, lds_kv);
-    if (e == hipSuccess) e = set_lds(attn_bwd_dq_f32_kernel<DH>, lds_q);
-    if (e != hipSuccess) return e;
     const unsigned tiles = (unsigned)(a.Sp / 64);
-    hipLaunchKernelGGL(attn_bwd_dkdv_f32_kernel<DH>, dim3(tiles, a.H, a.B), dim3(64), lds_kv, s, a);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_bwd_dq_f32_kernel<DH>, dim3(tiles, a.H, a.B), dim3(64), lds_q, s, a);
+    if (part == 0) {
+      const int lds = (2 * DH * 65 + 2 * 16 * DH + 32) * 4;
+      hipError_t e = set_lds(attn_bwd_dkdv_f32_kernel<DH>, lds);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(attn_bwd_dkdv_f32_kernel<DH>, dim3(tiles, a.H, a.B), dim3(64), lds, s, a);
+    } else {
+      const int lds = (2 * DH * 65 + 2 * 16 * DH) * 4;
+      hipError_t e = set_lds(attn_bwd_dq_f32_kernel<DH>, lds);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(attn_bwd_dq_f32_kernel<DH>, dim3(tiles, a.H, a.B), dim3(64), lds, s, a);
+    }
   }
   return hipGetLastError();
 }
@@ -800,9 +805,9 @@ hipError_t attn_fwd(Dt dt, const AttnArgs& a, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-hipError_t attn_bwd(Dt dt, const AttnArgs& a, hipStream_t s) {
-  if (a.dh == 64) return bwd_launch<64>(dt, a, s);
-  if (a.dh == 128) return bwd_launch<128>(dt, a, s);
+hipError_t attn_bwd(Dt dt, int part, const AttnArgs& a, hipStream_t s) {
+  if (a.dh == 64) return bwd_launch<64>(dt, part, a, s);
+  if (a.dh == 128) return bwd_launch<128>(dt, part, a, s);
   return hipErrorInvalidValue;
 }
 

@@ -61,7 +61,8 @@ struct AttnArgs {
 };
 
 hipError_t attn_fwd(Dt dt, const AttnArgs& a, hipStream_t s);
-hipError_t attn_bwd(Dt dt, const AttnArgs& a, hipStream_t s);
+// part 0: dK and dV (key-outer kernel); part 1: dQ (query-outer kernel)
+hipError_t attn_bwd(Dt dt, int part, const AttnArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- row-wise / layout kernels
 // LayerNorm over D per row. x: [rows, D] (ti); out [rows, D] (to).

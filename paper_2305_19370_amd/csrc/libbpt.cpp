@@ -7,7 +7,10 @@
 #include <string.h>
 
 #include <algorithm>
+#include <map>
+#include <mutex>
 #include <string>
+#include <vector>
 
 #include "../../include/libbpt.h"
 #include "internal.h"
@@ -187,6 +190,61 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 char* off(const void* p, int64_t bytes) { return (char*)p + bytes; }
 
+
+// ---------------------------------------------------------------- launch profiler
+// Off by default. When on, every launch of bpt_layer_fwd / bpt_layer_bwd is
+// bracketed by two HIP events recorded on the launch stream, tagged with the
+// call site's name and its algorithmic flops / HBM bytes.
+struct ProfRec {
+  std::string name;
+  double flops, bytes;
+  hipEvent_t a, b;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof;
+std::vector<hipEvent_t> g_pool;
+size_t g_pool_used = 0;
+
+hipEvent_t pool_event() {
+  if (g_pool_used == g_pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    g_pool.push_back(e);
+  }
+  return g_pool[g_pool_used++];
+}
+
+template <class Fn>
+hipError_t launch(const char* name, double flops, double bytes, hipStream_t s, Fn&& fn) {
+  if (!g_prof_on) return fn();
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  hipEvent_t a = pool_event(), b = pool_event();
+  if (!a || !b) return fn();
+  hipEventRecord(a, s);
+  hipError_t e = fn();
+  hipEventRecord(b, s);
+  g_prof.push_back({name, flops, bytes, a, b});
+  return e;
+}
+
+#define RUN(name, flops, bytes, expr)                                                        \
+  do {                                                                                       \
+    hipError_t _e = launch(name, (double)(flops), (double)(bytes), s, [&] { return (expr); }); \
+    if (_e != hipSuccess) return fail(BPT_ERR_HIP, "%s: %s", name, hipGetErrorString(_e));  \
+  } while (0)
+
+double gemm_flops(const GemmArgs& g) { return 2.0 * g.M * g.N * g.K * g.batch; }
+double gemm_bytes(const GemmArgs& g, size_t eab, size_t ec) {
+  const double ncols = (double)std::max(g.N, g.Nstore);
+  return ((double)g.M * g.K + (double)g.N * g.K) * eab * g.batch + (double)g.M * ncols * ec * g.batch;
+}
+// visible (query, key) pairs of query rows [q0, q1) of one sequence of length S
+double attn_pairs(int64_t q0, int64_t q1, int64_t S, int causal) {
+  if (!causal) return (double)(q1 - q0) * S;
+  return 0.5 * ((double)q1 * (q1 + 1) - (double)q0 * (q0 + 1));
+}
+
 }  // namespace
 
 extern "C" {
@@ -210,8 +268,7 @@ bpt_status bpt_saved_layout_of(const bpt_config* cfg, bpt_saved_layout* out) {
   if (st != BPT_OK) return st;
   if (!out) return fail(BPT_ERR_INVALID_ARG, "out is NULL");
   int64_t total;
-  SavedPtrs s = saved_layout(dims_of(*cfg), nullptr, &total);
-  // with a null base every pointer equals its byte offset
+  SavedPtrs s = saved_layout(dims_of(*cfg), nullptr, &total);   // zero base: pointers are offsets
   out->qk = (size_t)(uintptr_t)s.qk;
   out->vt = (size_t)(uintptr_t)s.vt;
   out->o = (size_t)(uintptr_t)s.o;
@@ -266,6 +323,48 @@ size_t bpt_describe(const bpt_config* cfg, char* buf, size_t n) {
   return w < 0 ? 0 : std::min((size_t)w, n - 1);
 }
 
+bpt_status bpt_profile_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (on) {             // start a new record; turning off keeps it for bpt_profile_report
+    g_prof.clear();
+    g_pool_used = 0;
+  }
+  g_prof_on = on != 0;
+  return BPT_OK;
+}
+
+size_t bpt_profile_report(char* buf, size_t n) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  struct Agg { int count = 0; double ms = 0, flops = 0, bytes = 0; };
+  std::map<std::string, Agg> agg;
+  for (const ProfRec& r : g_prof) {
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) ms = -1.0f;
+    Agg& a = agg[r.name];
+    a.count += 1;
+    a.ms += ms;
+    a.flops += r.flops;
+    a.bytes += r.bytes;
+  }
+  std::string out = "{";
+  bool first = true;
+  for (auto& kv : agg) {
+    char line[512];
+    snprintf(line, sizeof line, "%s\"%s\": {\"count\": %d, \"ms\": %.6f, \"flops\": %.6e, \"bytes\": %.6e}",
+             first ? "" : ", ", kv.first.c_str(), kv.second.count, kv.second.ms, kv.second.flops,
+             kv.second.bytes);
+    out += line;
+    first = false;
+  }
+  out += "}";
+  if (buf && n > 0) {
+    const size_t k = std::min(out.size(), n - 1);
+    memcpy(buf, out.data(), k);
+    buf[k] = 0;
+  }
+  return out.size();
+}
+
 bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params* p, void* Y, void* saved,
                          void* ws, size_t ws_bytes, void* stream) {
   bpt_status st = check(cfg);
@@ -288,22 +387,25 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
   const Dt E = cfg->dtype == BPT_BF16 ? BF16 : F32;
   const Dt OUT = cfg->out_dtype == BPT_BF16 ? BF16 : F32;
   const int64_t D = d.D, F = d.F, T = d.T, E_ = (int64_t)d.E;
+  const size_t EO = esize(cfg->out_dtype);
 
   // weights into the K-contiguous layouts the NT GEMMs read
-  HIPCHK(transpose(E, p->Wq, D, 0, w.wqkT, D, 0, D, D, D, 1, s));
-  HIPCHK(transpose(E, p->Wk, D, 0, off(w.wqkT, D * D * E_), D, 0, D, D, D, 1, s));
-  HIPCHK(transpose(E, p->Wv, D, 0, w.wvT, D, 0, D, D, D, 1, s));
-  HIPCHK(transpose(E, p->Wo, D, 0, w.woT, D, 0, D, D, D, 1, s));
-  HIPCHK(transpose(E, p->W1, F, 0, w.w1T, D, 0, D, F, D, 1, s));
-  HIPCHK(transpose(E, p->W2, D, 0, w.w2T, F, 0, F, D, F, 1, s));
+  const double wb = 2.0 * E_;
+  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wq, D, 0, w.wqkT, D, 0, D, D, D, 1, s));
+  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wk, D, 0, off(w.wqkT, D * D * E_), D, 0, D, D, D, 1, s));
+  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wv, D, 0, w.wvT, D, 0, D, D, D, 1, s));
+  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wo, D, 0, w.woT, D, 0, D, D, D, 1, s));
+  RUN("transpose.weights", 0, wb * D * F, transpose(E, p->W1, F, 0, w.w1T, D, 0, D, F, D, 1, s));
+  RUN("transpose.weights", 0, wb * D * F, transpose(E, p->W2, D, 0, w.w2T, F, 0, F, D, F, 1, s));
 
   // U = LN1(X); [Q | K] = U [Wq | Wk]; V^T = Wv^T U^T  (Algorithm 1: project the input)
-  HIPCHK(layer_norm(E, E, X, D, p->ln1_g, p->ln1_b, w.u, D, sv.mu1, sv.rstd1, T, D, cfg->ln_eps, 0, s));
+  RUN("layernorm.fwd", 0, 2.0 * T * D * E_,
+      layer_norm(E, E, X, D, p->ln1_g, p->ln1_b, w.u, D, sv.mu1, sv.rstd1, T, D, cfg->ln_eps, 0, s));
   {
     GemmArgs g;
     g.A = w.u; g.lda = D; g.B = w.wqkT; g.ldb = D; g.C = sv.qk; g.ldc = 2 * D;
     g.M = T; g.N = 2 * D; g.K = D;
-    HIPCHK(gemm(E, EPI_STORE, E, F32, g, s));
+    RUN("gemm.qk", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
   }
   {
     GemmArgs g;
@@ -311,7 +413,7 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
     g.B = w.u; g.ldb = D; g.sB = d.S * D;
     g.C = sv.vt; g.ldc = d.Tp; g.sC = d.Sp;
     g.M = D; g.N = d.S; g.Nstore = d.Sp; g.K = D; g.batch = (int)d.B;
-    HIPCHK(gemm(E, EPI_STORE, E, F32, g, s));
+    RUN("gemm.vt", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
   }
 
   // Outer loop over groups of query blocks: attention for the group, then the
@@ -328,26 +430,29 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
       a.lse = sv.lse;
       a.S = d.S; a.Sp = d.Sp; a.B = (int)d.B; a.H = (int)d.H; a.dh = (int)d.dh; a.causal = cfg->causal;
       a.q_begin = s0; a.q_end = s0 + r; a.b_begin = (int)b; a.nb = 1;
-      HIPCHK(attn_fwd(E, a, s));
+      const double pairs = attn_pairs(s0, s0 + r, d.S, cfg->causal) * d.H;
+      RUN("attn.fwd", 4.0 * d.dh * pairs, (3.0 * r + 2.0 * (s0 + r)) * D * E_, attn_fwd(E, a, s));
 
       GemmArgs go;     // h = X + O Wo
       go.A = off(sv.o, t0 * D * E_); go.lda = D; go.B = w.woT; go.ldb = D;
       go.C = sv.h + t0 * D; go.ldc = D; go.R = off(X, t0 * D * E_); go.ldr = D;
       go.M = r; go.N = D; go.K = D;
-      HIPCHK(gemm(E, EPI_RESID, F32, E, go, s));
+      RUN("gemm.wo", gemm_flops(go), gemm_bytes(go, E_, 4) + (double)r * D * E_,
+          gemm(E, EPI_RESID, F32, E, go, s));
 
-      HIPCHK(layer_norm(F32, E, sv.h + t0 * D, D, p->ln2_g, p->ln2_b, w.vg, D, sv.mu2 + t0, sv.rstd2 + t0, r,
-                        D, cfg->ln_eps, 0, s));
+      RUN("layernorm.fwd", 0, (double)r * D * (4 + E_),
+          layer_norm(F32, E, sv.h + t0 * D, D, p->ln2_g, p->ln2_b, w.vg, D, sv.mu2 + t0, sv.rstd2 + t0, r,
+                     D, cfg->ln_eps, 0, s));
 
       GemmArgs g1;     // G = GELU(LN2(h) W1 + b1)
       g1.A = w.vg; g1.lda = D; g1.B = w.w1T; g1.ldb = D; g1.C = w.gg; g1.ldc = F;
       g1.bias = p->b1; g1.M = r; g1.N = F; g1.K = D;
-      HIPCHK(gemm(E, EPI_GELU, E, F32, g1, s));
+      RUN("gemm.ffn1", gemm_flops(g1), gemm_bytes(g1, E_, E_), gemm(E, EPI_GELU, E, F32, g1, s));
 
       GemmArgs g2;     // Y = h + G W2 + b2
-      g2.A = w.gg; g2.lda = F; g2.B = w.w2T; g2.ldb = F; g2.C = off(Y, t0 * D * esize(cfg->out_dtype));
+      g2.A = w.gg; g2.lda = F; g2.B = w.w2T; g2.ldb = F; g2.C = off(Y, t0 * D * EO);
       g2.ldc = D; g2.R = sv.h + t0 * D; g2.ldr = D; g2.bias = p->b2; g2.M = r; g2.N = D; g2.K = F;
-      HIPCHK(gemm(E, EPI_RESID, OUT, F32, g2, s));
+      RUN("gemm.ffn2", gemm_flops(g2), gemm_bytes(g2, E_, EO) + 4.0 * r * D, gemm(E, EPI_RESID, OUT, F32, g2, s));
     }
   }
   return BPT_OK;
@@ -380,12 +485,14 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
   const Dt E = cfg->dtype == BPT_BF16 ? BF16 : F32;
   const Dt OUT = cfg->out_dtype == BPT_BF16 ? BF16 : F32;
   const int64_t D = d.D, F = d.F, T = d.T, Tp = d.Tp, Sp = d.Sp, S = d.S, E_ = (int64_t)d.E;
+  const size_t EO = esize(cfg->out_dtype);
   const int B = (int)d.B;
+  const double tb = 2.0 * E_;   // bytes per element of a transpose / copy (read + write)
 
-  HIPCHK(transpose(E, p->W1, F, 0, w.w1T, D, 0, D, F, D, 1, s));
-  HIPCHK(copy2d(E, p->Wq, D, w.wcat, 3 * D, D, D, s));
-  HIPCHK(copy2d(E, p->Wk, D, off(w.wcat, D * E_), 3 * D, D, D, s));
-  HIPCHK(copy2d(E, p->Wv, D, off(w.wcat, 2 * D * E_), 3 * D, D, D, s));
+  RUN("transpose.weights", 0, tb * D * F, transpose(E, p->W1, F, 0, w.w1T, D, 0, D, F, D, 1, s));
+  RUN("copy.weights", 0, tb * D * D, copy2d(E, p->Wq, D, w.wcat, 3 * D, D, D, s));
+  RUN("copy.weights", 0, tb * D * D, copy2d(E, p->Wk, D, off(w.wcat, D * E_), 3 * D, D, D, s));
+  RUN("copy.weights", 0, tb * D * D, copy2d(E, p->Wv, D, off(w.wcat, 2 * D * E_), 3 * D, D, D, s));
 
   // ---- FFN and LN2 backward, per group of query blocks, recomputing the FFN intermediate
   bool first = true;
@@ -393,72 +500,75 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     for (int64_t s0 = 0; s0 < S; s0 += d.R) {
       const int64_t r = std::min(d.R, S - s0), rp = rup(r, 64), t0 = b * S + s0;
       const void* dYg = off(dY, t0 * D * E_);
-      HIPCHK(layer_norm(F32, E, sv.h + t0 * D, D, p->ln2_g, p->ln2_b, w.vg, D, sv.mu2 + t0, sv.rstd2 + t0, r,
-                        D, cfg->ln_eps, 1, s));
+      RUN("layernorm.fwd", 0, (double)r * D * (4 + E_),
+          layer_norm(F32, E, sv.h + t0 * D, D, p->ln2_g, p->ln2_b, w.vg, D, sv.mu2 + t0, sv.rstd2 + t0, r, D,
+                     cfg->ln_eps, 1, s));
       {   // Z^T = W1^T v^T: G^T = GELU(Z^T + b1), GELU'(Z^T)
         GemmArgs g;
         g.A = w.w1T; g.lda = D; g.B = w.vg; g.ldb = D; g.C = w.gT; g.ldc = d.Rp; g.C2 = w.gpT; g.ldc2 = d.Rp;
         g.bias = p->b1; g.bias_on_m = 1; g.M = F; g.N = r; g.Nstore = rp; g.K = D;
-        HIPCHK(gemm(E, EPI_GELU, E, F32, g, s));
+        RUN("gemm.bwd_ffn1_recompute", gemm_flops(g), gemm_bytes(g, E_, E_ + 4), gemm(E, EPI_GELU, E, F32, g, s));
       }
       {   // dZ^T = (W2 dY^T) * GELU'(Z^T)
         GemmArgs g;
         g.A = p->W2; g.lda = D; g.B = dYg; g.ldb = D; g.C = w.dzT; g.ldc = d.Rp; g.R = w.gpT; g.ldr = d.Rp;
         g.M = F; g.N = r; g.Nstore = rp; g.K = D;
-        HIPCHK(gemm(E, EPI_MUL, E, F32, g, s));
+        RUN("gemm.bwd_dz", gemm_flops(g), gemm_bytes(g, E_, E_ + 4), gemm(E, EPI_MUL, E, F32, g, s));
       }
-      if (G.db1) HIPCHK(row_sum(E, w.dzT, d.Rp, F, r, G.db1, first ? 0 : 1, s));
+      if (G.db1) RUN("reduce.bias", 0, (double)F * r * E_, row_sum(E, w.dzT, d.Rp, F, r, G.db1, first ? 0 : 1, s));
       if (G.dW2) {   // dW2 = G^T dY
-        HIPCHK(transpose(E, dYg, D, 0, w.dyT, d.Rp, 0, r, D, rp, 1, s));
+        RUN("transpose.act", 0, tb * r * D, transpose(E, dYg, D, 0, w.dyT, d.Rp, 0, r, D, rp, 1, s));
         GemmArgs g;
         g.A = w.gT; g.lda = d.Rp; g.B = w.dyT; g.ldb = d.Rp; g.C = G.dW2; g.ldc = D;
         g.M = F; g.N = D; g.K = rp; g.accumulate = first ? 0 : 1;
-        HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+        RUN("gemm.bwd_dw2", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
       }
-      HIPCHK(transpose(E, w.dzT, d.Rp, 0, w.dz, F, 0, F, r, F, 1, s));
+      RUN("transpose.act", 0, tb * r * F, transpose(E, w.dzT, d.Rp, 0, w.dz, F, 0, F, r, F, 1, s));
       {   // dv = dZ W1^T
         GemmArgs g;
         g.A = w.dz; g.lda = F; g.B = p->W1; g.ldb = F; g.C = w.dv + t0 * D; g.ldc = D;
         g.M = r; g.N = D; g.K = F;
-        HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+        RUN("gemm.bwd_dv", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
       }
       if (G.dW1) {   // dW1 = v^T dZ
-        HIPCHK(transpose(E, w.vg, D, 0, w.vgT, d.Rp, 0, r, D, rp, 1, s));
+        RUN("transpose.act", 0, tb * r * D, transpose(E, w.vg, D, 0, w.vgT, d.Rp, 0, r, D, rp, 1, s));
         GemmArgs g;
         g.A = w.vgT; g.lda = d.Rp; g.B = w.dzT; g.ldb = d.Rp; g.C = G.dW1; g.ldc = F;
         g.M = D; g.N = F; g.K = rp; g.accumulate = first ? 0 : 1;
-        HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+        RUN("gemm.bwd_dw1", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
       }
       first = false;
     }
   }
   // dh = dY + LN2^T(dv)
-  HIPCHK(layer_norm_bwd(F32, sv.h, sv.mu2, sv.rstd2, p->ln2_g, w.dv, E, dY, F32, w.dh, E, w.dhe, T, D, s));
+  RUN("layernorm.bwd", 0, (double)T * D * (4 + 4 + E_ + 4 + E_),
+      layer_norm_bwd(F32, sv.h, sv.mu2, sv.rstd2, p->ln2_g, w.dv, E, dY, F32, w.dh, E, w.dhe, T, D, s));
   if (G.dln2_g || G.dln2_b)
-    HIPCHK(layer_norm_param_grad(F32, sv.h, sv.mu2, sv.rstd2, w.dv, G.dln2_g ? G.dln2_g : w.scratch,
-                                 G.dln2_b ? G.dln2_b : w.scratch + D, w.partial, T, D, s));
-  if (G.db2) HIPCHK(col_sum(E, dY, D, T, D, G.db2, 0, w.partial, s));
+    RUN("reduce.layernorm", 0, (double)T * D * 8,
+        layer_norm_param_grad(F32, sv.h, sv.mu2, sv.rstd2, w.dv, G.dln2_g ? G.dln2_g : w.scratch,
+                              G.dln2_b ? G.dln2_b : w.scratch + D, w.partial, T, D, s));
+  if (G.db2) RUN("reduce.bias", 0, (double)T * D * E_, col_sum(E, dY, D, T, D, G.db2, 0, w.partial, s));
 
   // ---- output projection backward: dO = dh Wo^T, dWo = O^T dh
   {
     GemmArgs g;
     g.A = w.dhe; g.lda = D; g.B = p->Wo; g.ldb = D; g.C = w.dO; g.ldc = D; g.M = T; g.N = D; g.K = D;
-    HIPCHK(gemm(E, EPI_STORE, E, F32, g, s));
+    RUN("gemm.bwd_do", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
   }
   if (G.dWo) {
-    HIPCHK(transpose(E, sv.o, D, S * D, w.oT, Tp, Sp, S, D, Sp, B, s));
-    HIPCHK(transpose(E, w.dhe, D, S * D, w.dhT, Tp, Sp, S, D, Sp, B, s));
+    RUN("transpose.act", 0, tb * T * D, transpose(E, sv.o, D, S * D, w.oT, Tp, Sp, S, D, Sp, B, s));
+    RUN("transpose.act", 0, tb * T * D, transpose(E, w.dhe, D, S * D, w.dhT, Tp, Sp, S, D, Sp, B, s));
     GemmArgs g;
     g.A = w.oT; g.lda = Tp; g.B = w.dhT; g.ldb = Tp; g.C = G.dWo; g.ldc = D; g.M = D; g.N = D; g.K = Tp;
-    HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+    RUN("gemm.bwd_dwo", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
   }
 
   // ---- attention backward, probabilities rebuilt from the saved log-sum-exp
-  HIPCHK(attn_delta(E, w.dO, sv.o, D, w.delta, B, S, Sp, (int)d.H, (int)d.dh, s));
-  HIPCHK(transpose(E, sv.vt, Tp, Sp, w.V, D, S * D, D, S, D, B, s));
-  HIPCHK(transpose(E, sv.qk, 2 * D, S * 2 * D, w.qT, Tp, Sp, S, D, Sp, B, s));
-  HIPCHK(transpose(E, off(sv.qk, D * E_), 2 * D, S * 2 * D, w.kT, Tp, Sp, S, D, Sp, B, s));
-  HIPCHK(transpose(E, w.dO, D, S * D, w.dOT, Tp, Sp, S, D, Sp, B, s));
+  RUN("attn.delta", 0, 2.0 * T * D * E_, attn_delta(E, w.dO, sv.o, D, w.delta, B, S, Sp, (int)d.H, (int)d.dh, s));
+  RUN("transpose.act", 0, tb * T * D, transpose(E, sv.vt, Tp, Sp, w.V, D, S * D, D, S, D, B, s));
+  RUN("transpose.act", 0, tb * T * D, transpose(E, sv.qk, 2 * D, S * 2 * D, w.qT, Tp, Sp, S, D, Sp, B, s));
+  RUN("transpose.act", 0, tb * T * D, transpose(E, off(sv.qk, D * E_), 2 * D, S * 2 * D, w.kT, Tp, Sp, S, D, Sp, B, s));
+  RUN("transpose.act", 0, tb * T * D, transpose(E, w.dO, D, S * D, w.dOT, Tp, Sp, S, D, Sp, B, s));
   {
     AttnArgs a;
     a.q = sv.qk; a.ld_q = 2 * D;
@@ -471,33 +581,40 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     a.dqt = w.dqkvT; a.dkt = off(w.dqkvT, D * Tp * E_); a.dvt = off(w.dqkvT, 2 * D * Tp * E_); a.ld_dt = Tp;
     a.lse = sv.lse; a.delta = w.delta;
     a.S = S; a.Sp = Sp; a.B = B; a.H = (int)d.H; a.dh = (int)d.dh; a.causal = cfg->causal;
-    HIPCHK(attn_bwd(E, a, s));
+    const double pairs = attn_pairs(0, S, S, cfg->causal) * d.H * B;
+    // key-outer: S = Q K^T, dP = dO V^T, dV += P^T dO, dK += dS^T Q (4 contractions)
+    RUN("attn.bwd_dkdv", 8.0 * d.dh * pairs, 8.0 * T * D * E_, attn_bwd(E, 0, a, s));
+    // query-outer: S^T, dP^T, dQ += dS K (3 contractions)
+    RUN("attn.bwd_dq", 6.0 * d.dh * pairs, 6.0 * T * D * E_, attn_bwd(E, 1, a, s));
   }
 
   // ---- QKV projection and LN1 backward
-  HIPCHK(transpose(E, w.dqkvT, Tp, Sp, w.dqkv, 3 * D, S * 3 * D, 3 * D, S, 3 * D, B, s));
+  RUN("transpose.act", 0, tb * 3 * T * D, transpose(E, w.dqkvT, Tp, Sp, w.dqkv, 3 * D, S * 3 * D, 3 * D, S, 3 * D, B, s));
   if (G.dWq || G.dWk || G.dWv) {
-    HIPCHK(layer_norm(E, E, X, D, p->ln1_g, p->ln1_b, w.u, D, sv.mu1, sv.rstd1, T, D, cfg->ln_eps, 1, s));
-    HIPCHK(transpose(E, w.u, D, S * D, w.uT, Tp, Sp, S, D, Sp, B, s));
+    RUN("layernorm.fwd", 0, 2.0 * T * D * E_,
+        layer_norm(E, E, X, D, p->ln1_g, p->ln1_b, w.u, D, sv.mu1, sv.rstd1, T, D, cfg->ln_eps, 1, s));
+    RUN("transpose.act", 0, tb * T * D, transpose(E, w.u, D, S * D, w.uT, Tp, Sp, S, D, Sp, B, s));
     float* outs[3] = {G.dWq, G.dWk, G.dWv};
     for (int i = 0; i < 3; ++i) {
       if (!outs[i]) continue;
       GemmArgs g;
       g.A = w.uT; g.lda = Tp; g.B = off(w.dqkvT, i * D * Tp * E_); g.ldb = Tp; g.C = outs[i]; g.ldc = D;
       g.M = D; g.N = D; g.K = Tp;
-      HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+      RUN("gemm.bwd_dwqkv", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
     }
   }
   {
     GemmArgs g;   // dU = [dQ dK dV] [Wq Wk Wv]^T
     g.A = w.dqkv; g.lda = 3 * D; g.B = w.wcat; g.ldb = 3 * D; g.C = w.dU; g.ldc = D; g.M = T; g.N = D;
     g.K = 3 * D;
-    HIPCHK(gemm(E, EPI_STORE, F32, F32, g, s));
+    RUN("gemm.bwd_du", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
   }
-  HIPCHK(layer_norm_bwd(E, X, sv.mu1, sv.rstd1, p->ln1_g, w.dU, F32, w.dh, OUT, dX, OUT, nullptr, T, D, s));
+  RUN("layernorm.bwd", 0, (double)T * D * (E_ + 4 + 4 + EO),
+      layer_norm_bwd(E, X, sv.mu1, sv.rstd1, p->ln1_g, w.dU, F32, w.dh, OUT, dX, OUT, nullptr, T, D, s));
   if (G.dln1_g || G.dln1_b)
-    HIPCHK(layer_norm_param_grad(E, X, sv.mu1, sv.rstd1, w.dU, G.dln1_g ? G.dln1_g : w.scratch,
-                                 G.dln1_b ? G.dln1_b : w.scratch + D, w.partial, T, D, s));
+    RUN("reduce.layernorm", 0, (double)T * D * (E_ + 4),
+        layer_norm_param_grad(E, X, sv.mu1, sv.rstd1, w.dU, G.dln1_g ? G.dln1_g : w.scratch,
+                              G.dln1_b ? G.dln1_b : w.scratch + D, w.partial, T, D, s));
   return BPT_OK;
 }
 

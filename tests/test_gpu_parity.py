@@ -2,38 +2,50 @@
 seeded inputs. Shapes span several tiles with ragged tails; both causal and
 non-causal; fp32 and bf16 paths; LayerNorm affine parameters and FFN biases on.
 
-Gates (written in each test):
-  fp32: normwise max|diff| <= 1e-4 * max|ref| and elementwise relative error
-        <= 1e-4 wherever |ref| >= 1e-2 * rms(ref);
-  bf16: e_max = max|diff| / rms(ref) <= 2e-2 and e_mean = mean|diff| / rms(ref)
-        <= 2e-3 for outputs, attention intermediates and dX; weight gradients
-        (sums over every token of products of bf16-rounded operands) are held to
-        e_max <= 4e-2, e_mean <= 4e-3.
+Gates (written in each test; e_max = max|diff| / rms(ref), e_mean = mean|diff| / rms(ref),
+with ref the float64 oracle):
+  fp32: e_max <= 1e-4 for every output and gradient (max|diff| <= 1e-4 * rms(ref),
+        which also bounds the normwise relative error max|diff| / max|ref|);
+  bf16: e_max <= max(2e-2, 1.25 * e_max of the bf16 rounding model) and
+        e_mean <= max(2e-3, 1.25 * e_mean of the rounding model), per tensor.
+        The rounding model (oracle/bf16_model.py) is the same definition with
+        every matrix-multiply operand rounded to bf16: what any bf16-operand
+        implementation lands at on this input. For most tensors the first term
+        decides; the weight gradients and, with the causal mask, dX carry the
+        bf16 floor above 2e-2 / 2e-3.
 """
 import numpy as np
 import pytest
 import torch
 
 from bpt_inputs import WORKLOADS, make_inputs, small_workload
-from gpu_util import GRAD_NAMES, fp32_ok, run_gpu, run_oracle, say, stats, table
+from gpu_util import GRAD_NAMES, bf16_model, run_gpu, run_oracle, say, stats, table
 
 pytestmark = pytest.mark.gpu
 
-BF16_OUT = dict(e_max=2e-2, e_mean=2e-3)
-BF16_WGRAD = dict(e_max=4e-2, e_mean=4e-3)
+FP32_E_MAX = 1e-4
+BF16_E_MAX, BF16_E_MEAN, MODEL_FACTOR = 2e-2, 2e-3, 1.25
+
+
+def bf16_limits(model_stats):
+    return (max(BF16_E_MAX, MODEL_FACTOR * model_stats["e_max"]),
+            max(BF16_E_MEAN, MODEL_FACTOR * model_stats["e_mean"]))
 
 
 def compare_all(w, inp, gpu, Yr, g, tol_kind, label):
     rows, bad = [], []
     names = ["Y", "dX"] + [n for n in GRAD_NAMES if n in gpu]
+    model = bf16_model(w, inp) if tol_kind == "bf16" else None
     for n in names:
         ref = Yr if n == "Y" else g[n]
+        s = stats(gpu[n].numpy(), ref)
         if tol_kind == "fp32":
-            ok, s = fp32_ok(gpu[n].numpy(), ref)
+            ok = s["e_max"] <= FP32_E_MAX
         else:
-            s = stats(gpu[n].numpy(), ref)
-            lim = BF16_OUT if n in ("Y", "dX", "dln1_g", "dln1_b", "dln2_g", "dln2_b", "db1", "db2") else BF16_WGRAD
-            ok = s["e_max"] <= lim["e_max"] and s["e_mean"] <= lim["e_mean"]
+            ms = stats(model[n], ref)
+            lim_max, lim_mean = bf16_limits(ms)
+            s["lim_max"], s["lim_mean"] = lim_max, lim_mean
+            ok = s["e_max"] <= lim_max and s["e_mean"] <= lim_mean
         rows.append((n, s))
         if not ok:
             bad.append(n)
@@ -96,11 +108,17 @@ def test_bf16_saved_intermediates():
         "rstd2": (sv["rstd2"].reshape(B, S), c["rstd2"][..., 0]),
         "Y": (gpu["Y"], Yr),
     }
+    model = bf16_model(w, inp)
+    model_of = {"O": model["O"], "lse": model["lse"], "h": model["Hd"], "Y": model["Y"]}
     rows, bad = [], []
     for n, (got, ref) in checks.items():
         s = stats(got.numpy(), ref)
+        lim_max, lim_mean = BF16_E_MAX, BF16_E_MEAN
+        if n in model_of:
+            lim_max, lim_mean = bf16_limits(stats(model_of[n], ref))
+        s["lim_max"], s["lim_mean"] = lim_max, lim_mean
         rows.append((n, s))
-        if not (s["e_max"] <= 2e-2 and s["e_mean"] <= 2e-3):
+        if not (s["e_max"] <= lim_max and s["e_mean"] <= lim_mean):
             bad.append(n)
     assert torch.all(vt[:, :, S:] == 0), "padding columns of V^T must be zero"
     say("\n" + table(rows))

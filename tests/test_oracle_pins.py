@@ -388,3 +388,36 @@ def test_rows_oracle_matches_full(causal):
     Yr2, none = oracle.rows_layer_fwd_bwd(X, p, H, causal, rows, None, EPS)
     assert none is None
     np.testing.assert_array_equal(Yr2, Yr)
+
+
+# ----------------------------------------------------------------------------- bf16 rounding model
+def test_bf16_rounding_matches_torch():
+    from oracle.bf16_model import to_bf16
+    rng = np.random.default_rng(15)
+    x = np.concatenate([rng.normal(size=4000) * 10 ** rng.uniform(-6, 6, 4000),
+                        np.array([0.0, -0.0, 1.0, 1.00390625, 1.01171875, -3.0e38, 1e-40])])
+    x32 = x.astype(np.float32)
+    ref = torch.from_numpy(x32).to(torch.bfloat16).double().numpy()
+    np.testing.assert_array_equal(to_bf16(x32.astype(np.float64)), ref)
+    # ties go to even: 1 + 2^-8 lies halfway between 1 and 1 + 2^-7
+    assert to_bf16(np.array([1.0 + 2 ** -8]))[0] == 1.0
+    assert to_bf16(np.array([1.0 + 3 * 2 ** -8]))[0] == 1.0 + 2 ** -6
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_bf16_model_without_rounding_is_the_oracle(causal):
+    from oracle.bf16_model import bf16_layer_fwd_bwd
+    rng = np.random.default_rng(16)
+    B, S, D, H, F = 2, 21, 16, 2, 32
+    p = rand_params(rng, D, F)
+    X, dY = rng.normal(size=(B, S, D)), rng.normal(size=(B, S, D))
+    Y, cache = layer_fwd(X, p, H, causal, EPS)
+    g = layer_bwd(cache, p, dY)
+    m = bf16_layer_fwd_bwd(X, p, H, causal, dY, EPS, round_operands=False)
+    np.testing.assert_allclose(m["Y"], Y, atol=1e-12)
+    np.testing.assert_allclose(m["O"], cache["O"], atol=1e-12)
+    for k in GRAD_OF:
+        np.testing.assert_allclose(m[k], g[k], atol=1e-11, err_msg=k)
+    mr = bf16_layer_fwd_bwd(X, p, H, causal, dY, EPS)     # rounding on: close, not equal
+    rel = np.abs(mr["Y"] - Y).max() / np.abs(Y).max()
+    assert 1e-5 < rel < 5e-2
