@@ -16,7 +16,14 @@ import tempfile
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
-SOURCES = ["libbpt.cpp", "gemm.hip", "attention.hip", "rowwise.hip"]
+SOURCES = ["libbpt.cpp", "gemm.hip", "attn_fwd.hip", "attn_bwd_dq.hip", "attn_bwd_dkdv.hip", "rowwise.hip"]
+# per-source code generation options: the backward attention kernels keep their
+# MFMA accumulators in architectural VGPRs (the default placement copies them
+# between register files every iteration)
+EXTRA_FLAGS = {
+    "attn_bwd_dq.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "attn_bwd_dkdv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
 LIB = os.path.join(PKG, "libbpt.so")
 ARCH = os.environ.get("BPT_OFFLOAD_ARCH", "gfx950")
 
@@ -36,7 +43,7 @@ def _hipcc() -> str:
 
 
 def _compile(src: str, obj: str) -> None:
-    cmd = [_hipcc(), *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *HIP_FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)

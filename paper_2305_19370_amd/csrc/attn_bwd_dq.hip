@@ -1,0 +1,225 @@
+// Attention backward, query-outer dQ kernel (bf16 MFMA and fp32 VALU variants).
+#include <algorithm>
+
+#include "attn_common.h"
+
+namespace bpt {
+
+// ====================================================================== backward dQ, bf16
+// Query-outer: per query tile, loop over key tiles; S^T = K Q^T, dP^T = V dO^T,
+// dS^T = P^T (dP^T - Delta), dQ^T += K^T dS^T.
+template <int DH>
+struct DqCfg {
+  static constexpr int KSTEPS = DH / 16, DT = DH / 32;
+  static constexpr int RBYTES = RmTile<DH>::BYTES, FBYTES = FmTile<DH>::BYTES;
+  static constexpr int STAGE = 2 * RBYTES + FBYTES;   // K, V row-major; K^T feature-major
+  static constexpr int LDS = 2 * STAGE;
+};
+
+template <int DH>
+__global__ __launch_bounds__(256, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
+  using C = DqCfg<DH>;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int S = (int)a.S;
+  const int qt = a.causal ? (int)gridDim.x - 1 - (int)blockIdx.x : (int)blockIdx.x;
+  const int q0 = qt * 128;
+  const int qw = q0 + 32 * wave;
+  const int qrow = qw + (lane & 31);
+  const float scale = rsqrtf((float)DH);
+  const float c = scale * LOG2E;
+
+  const bf16* Qb = (const bf16*)a.q + (int64_t)b * a.S * a.ld_q + h * DH;
+  const bf16* Kb = (const bf16*)a.k + (int64_t)b * a.S * a.ld_k + h * DH;
+  const bf16* Vb = (const bf16*)a.v + (int64_t)b * a.S * a.ld_v + h * DH;
+  const bf16* dOb = (const bf16*)a.dout + (int64_t)b * a.S * a.ld_do + h * DH;
+  const bf16* Ktb = (const bf16*)a.kt + (int64_t)h * DH * a.ld_kt + (int64_t)b * a.Sp;
+
+  bf16x8 qf[C::KSTEPS], dof[C::KSTEPS];
+  {
+    const int qr = qrow < S ? qrow : S - 1;
+#pragma unroll
+    for (int kk = 0; kk < C::KSTEPS; ++kk) {
+      qf[kk] = __builtin_bit_cast(bf16x8, ld16(Qb + (int64_t)qr * a.ld_q + 16 * kk + 8 * (lane >> 5)));
+      dof[kk] = __builtin_bit_cast(bf16x8, ld16(dOb + (int64_t)qr * a.ld_do + 16 * kk + 8 * (lane >> 5)));
+    }
+  }
+  const int64_t sidx = ((int64_t)b * a.H + h) * a.Sp + qrow;
+  const bool qok = qrow < S;
+  const float nlse2 = qok ? -a.lse2[sidx] : 0.0f;
+  const float dl = qok ? a.delta[sidx] : 0.0f;
+  // last key this lane's query may see (-1: none)
+  const int kv_last = !qok ? -1 : (a.causal ? qrow : S - 1);
+
+  const int kv_end = a.causal ? (q0 + 128 < S ? q0 + 128 : S) : S;
+  const int ntiles = (kv_end + 63) / 64;
+  DmaPlan<RmTile<DH>::BLOCKS> pk, pv;
+  DmaPlan<FmTile<DH>::BLOCKS> pkt;
+  plan_rows<DH>(pk, (int)a.ld_k, wave, lane);
+  plan_rows<DH>(pv, (int)a.ld_v, wave, lane);
+  plan_cols<DH>(pkt, (int)a.ld_kt, wave, lane);
+  auto issue = [&](int j) {
+    char* ks = smem + (j & 1) * C::STAGE;
+    dma_rows<DH>(ks, Kb, a.ld_k, j * 64, S - 1, wave, lane, pk);
+    dma_rows<DH>(ks + C::RBYTES, Vb, a.ld_v, j * 64, S - 1, wave, lane, pv);
+    dma_cols<DH>(ks + 2 * C::RBYTES, Ktb, j * 64, wave, pkt);
+  };
+
+  f32x16 acc[C::DT];
+#pragma unroll
+  for (int t = 0; t < C::DT; ++t) acc[t] = f32x16{};
+
+  auto tile = [&](int j, auto MASK) {
+    const int kv0 = j * 64;
+    const char* ks = smem + (j & 1) * C::STAGE;
+    const char* vs = ks + C::RBYTES;
+    const char* kts = vs + C::RBYTES;
+    const int lim = kv_last - kv0 - 4 * (lane >> 5);
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      f32x16 s = f32x16{}, dp = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < C::KSTEPS; ++kk) {
+        const int kc = 2 * kk + (lane >> 5);
+        const bf16x8 ak = *(const bf16x8*)(ks + rm_addr<DH>(32 * mt + (lane & 31), kc));
+        s = mfma32x32x16(ak, qf[kk], s);
+        const bf16x8 av = *(const bf16x8*)(vs + rm_addr<DH>(32 * mt + (lane & 31), kc));
+        dp = mfma32x32x16(av, dof[kk], dp);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float p = fast_exp2(fmaf(s[r], c, nlse2));
+        if constexpr (decltype(MASK)::value) p = (32 * mt + 8 * (r >> 2) + (r & 3) <= lim) ? p : 0.0f;
+        s[r] = p * (dp[r] - dl);                    // dS^T
+      }
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const bf16x8 sb = acc_to_b(s, hf);
+#pragma unroll
+        for (int t = 0; t < C::DT; ++t) {
+          const bf16x8 af = fm_frag<DH>(kts, 32 * t + (lane & 31), 32 * mt + 16 * hf, lane);
+          acc[t] = mfma32x32x16(af, sb, acc[t]);
+        }
+      }
+    }
+  };
+
+  // Key tiles every query of the workgroup fully sees come first (unmasked body);
+  // the diagonal and ragged tiles follow (masked body). Both loops are uniform over
+  // the workgroup, so every barrier is reached by all waves.
+  int n_full = a.causal ? std::min(ntiles, (q0 + 1) / 64) : ntiles;
+  n_full = std::min(n_full, S / 64);
+  if (q0 + 128 > S) n_full = 0;
+  if (ntiles > 0) issue(0);
+  wait_dma();
+  __syncthreads();
+  int j = 0;
+  for (; j < n_full; ++j) {
+    if (j + 1 < ntiles) issue(j + 1);
+    tile(j, std::false_type{});
+    wait_dma();
+    __syncthreads();
+  }
+  for (; j < ntiles; ++j) {
+    if (j + 1 < ntiles) issue(j + 1);
+    if (!(a.causal && j * 64 > qw + 31)) tile(j, std::true_type{});
+    wait_dma();
+    __syncthreads();
+  }
+
+  if (qrow < a.Sp) {
+    bf16* dQt = (bf16*)a.dqt + (int64_t)h * DH * a.ld_dt + (int64_t)b * a.Sp + qrow;
+#pragma unroll
+    for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int d = 32 * t + acc_row(r, lane);
+        dQt[(int64_t)d * a.ld_dt] = (bf16)(qok ? acc[t][r] * scale : 0.0f);
+      }
+  }
+}
+
+template <int DH>
+__global__ __launch_bounds__(64) void attn_bwd_dq_f32_kernel(AttnArgs a) {
+  extern __shared__ float fsm[];
+  float* Qown = fsm;                       // [DH][65]
+  float* dOown = Qown + DH * 65;           // [DH][65]
+  float* Ks = dOown + DH * 65;             // [16][DH]
+  float* Vs = Ks + 16 * DH;                // [16][DH]
+  const int tid = threadIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int64_t S = a.S, q0 = (int64_t)blockIdx.x * 64, q = q0 + tid;
+  const float scale = rsqrtf((float)DH);
+  const float* Qp = (const float*)a.q + (int64_t)h * DH;
+  const float* Kp = (const float*)a.k + (int64_t)h * DH;
+  const float* Vp = (const float*)a.v + (int64_t)h * DH;
+  const float* dOp = (const float*)a.dout + (int64_t)h * DH;
+  const int64_t sidx = ((int64_t)b * a.H + h) * a.Sp + q;
+  const float lq = q < S ? a.lse[sidx] : 0.0f;
+  const float dl = q < S ? a.delta[sidx] : 0.0f;
+  for (int d = 0; d < DH; ++d) {
+    Qown[d * 65 + tid] = q < S ? Qp[(b * S + q) * a.ld_q + d] : 0.0f;
+    dOown[d * 65 + tid] = q < S ? dOp[(b * S + q) * a.ld_do + d] : 0.0f;
+  }
+  float dq[DH];
+#pragma unroll
+  for (int d = 0; d < DH; ++d) dq[d] = 0.0f;
+  const int64_t kv_end = a.causal ? (q0 + 64 < S ? q0 + 64 : S) : S;
+  for (int64_t kv0 = 0; kv0 < kv_end; kv0 += 16) {
+    __syncthreads();
+    for (int i = tid; i < 16 * DH; i += 64) {
+      const int r = i / DH, d = i % DH;
+      const int64_t kv = kv0 + r;
+      Ks[i] = kv < S ? Kp[(b * S + kv) * a.ld_k + d] : 0.0f;
+      Vs[i] = kv < S ? Vp[(b * S + kv) * a.ld_v + d] : 0.0f;
+    }
+    __syncthreads();
+    for (int jj = 0; jj < 16; ++jj) {
+      const int64_t kv = kv0 + jj;
+      float sv = 0.0f, dpv = 0.0f;
+#pragma unroll
+      for (int d = 0; d < DH; ++d) {
+        sv = fmaf(Qown[d * 65 + tid], Ks[jj * DH + d], sv);
+        dpv = fmaf(dOown[d * 65 + tid], Vs[jj * DH + d], dpv);
+      }
+      const bool ok = q < S && kv < S && !(a.causal && kv > q);
+      const float p = ok ? __expf(sv * scale - lq) : 0.0f;
+      const float ds = p * (dpv - dl);
+#pragma unroll
+      for (int d = 0; d < DH; ++d) dq[d] = fmaf(ds, Ks[jj * DH + d], dq[d]);
+    }
+  }
+  if (q < a.Sp) {
+    float* dQt = (float*)a.dqt + (int64_t)h * DH * a.ld_dt + (int64_t)b * a.Sp + q;
+    const bool real = q < S;
+#pragma unroll
+    for (int d = 0; d < DH; ++d) dQt[(int64_t)d * a.ld_dt] = real ? dq[d] * scale : 0.0f;
+  }
+}
+
+
+template <int DH>
+static hipError_t dq_launch(Dt dt, const AttnArgs& a, hipStream_t s) {
+  if (a.S <= 0 || a.B <= 0) return hipSuccess;
+  if (dt == BF16) {
+    auto k = attn_bwd_dq_bf16_kernel<DH>;
+    hipError_t e = set_lds(k, DqCfg<DH>::LDS);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k, dim3((unsigned)((a.Sp + 127) / 128), a.H, a.B), dim3(256), DqCfg<DH>::LDS, s, a);
+  } else {
+    const int lds = (2 * DH * 65 + 2 * 16 * DH) * 4;
+    hipError_t e = set_lds(attn_bwd_dq_f32_kernel<DH>, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(attn_bwd_dq_f32_kernel<DH>, dim3((unsigned)(a.Sp / 64), a.H, a.B), dim3(64), lds, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t attn_bwd_dq(Dt dt, const AttnArgs& a, hipStream_t s) {
+  if (a.dh == 64) return dq_launch<64>(dt, a, s);
+  if (a.dh == 128) return dq_launch<128>(dt, a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace bpt

@@ -1,0 +1,275 @@
+// Blockwise attention for the BPT layer (paper, Section 3, eq. 3): for each query
+// tile, iterate over key/value tiles keeping a running row maximum and row sum,
+// rescale the running numerator by exp(old_max - new_max), and normalise once at
+// the end. The backward rebuilds each probability tile from the saved
+// log-sum-exp, P = exp(s - lse), so no S x S matrix is ever stored.
+//
+// bf16 kernels (gfx950 MFMA 32x32x16, fp32 accumulation, wave64):
+//  * scores are computed transposed, S^T[kv, q] = K Q^T, so that each lane owns a
+//    single query column: the row max / row sum of the softmax reduce over the
+//    lane's own accumulator registers plus one exchange with lane ^ 32;
+//  * the accumulator of S^T is, after exp and bf16 rounding, directly the B
+//    operand of O^T[d, q] += V^T[d, kv] P^T[kv, q] (the K index order inside one
+//    MFMA is permuted consistently on the A side), so P never touches LDS;
+//  * K and V^T tiles of 64 keys are staged in double-buffered LDS with a 16-byte
+//    chunk XOR swizzle; scores use exp2 with log2(e)/sqrt(dh) folded in one FMA.
+// fp32 kernels: one query (or key) row per thread with VALU FMAs; used by the
+// fp32 parity workload.
+#include <algorithm>
+
+#include "attn_common.h"
+
+namespace bpt {
+
+// ====================================================================== forward, bf16
+template <int DH>
+struct FwdCfg {
+  static constexpr int KSTEPS = DH / 16, DT = DH / 32;
+  static constexpr int KBYTES = RmTile<DH>::BYTES, VBYTES = FmTile<DH>::BYTES;
+  static constexpr int STAGE = KBYTES + VBYTES;
+  static constexpr int LDS = 2 * STAGE;
+};
+
+// Largest exponent growth (base 2) tolerated before the running numerator is
+// rescaled: exp-weights stay <= 2^8, and the final division uses the same
+// reference maximum, so the result is unchanged.
+static constexpr float RESCALE_LOG2 = 8.0f;
+
+template <int DH>
+__global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
+  using C = FwdCfg<DH>;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = blockIdx.y, b = a.b_begin + blockIdx.z;
+  const int S = (int)a.S;
+  // causal: the query tiles with the most keys are dispatched first
+  const int qt = a.causal ? (int)gridDim.x - 1 - (int)blockIdx.x : (int)blockIdx.x;
+  const int q0 = (int)a.q_begin + qt * 128;
+  const int qw = q0 + 32 * wave;
+  const int qrow = qw + (lane & 31);
+  const float scale = rsqrtf((float)DH);
+  const float c = scale * LOG2E;
+
+  const bf16* Qb = (const bf16*)a.q + (int64_t)b * a.S * a.ld_q + h * DH;
+  const bf16* Kb = (const bf16*)a.k + (int64_t)b * a.S * a.ld_k + h * DH;
+  const bf16* Vtb = (const bf16*)a.vt + (int64_t)h * DH * a.ld_vt + (int64_t)b * a.Sp;
+
+  bf16x8 qf[C::KSTEPS];
+  {
+    const int qr = qrow < S ? qrow : S - 1;
+#pragma unroll
+    for (int kk = 0; kk < C::KSTEPS; ++kk)
+      qf[kk] = __builtin_bit_cast(bf16x8, ld16(Qb + (int64_t)qr * a.ld_q + 16 * kk + 8 * (lane >> 5)));
+  }
+  // last key this lane's query may see
+  const int kv_last = a.causal ? (qrow < S - 1 ? qrow : S - 1) : S - 1;
+
+  const int kv_end = a.causal ? (q0 + 128 < S ? q0 + 128 : S) : S;
+  const int ntiles = (kv_end + 63) / 64;
+  DmaPlan<RmTile<DH>::BLOCKS> pk;
+  DmaPlan<FmTile<DH>::BLOCKS> pv;
+  plan_rows<DH>(pk, (int)a.ld_k, wave, lane);
+  plan_cols<DH>(pv, (int)a.ld_vt, wave, lane);
+  auto issue = [&](int j) {
+    char* kt = smem + (j & 1) * C::STAGE;
+    dma_rows<DH>(kt, Kb, a.ld_k, j * 64, S - 1, wave, lane, pk);
+    dma_cols<DH>(kt + C::KBYTES, Vtb, j * 64, wave, pv);
+  };
+
+  f32x16 acc[C::DT];
+#pragma unroll
+  for (int t = 0; t < C::DT; ++t) acc[t] = f32x16{};
+  float m_run = NEG_INF, l_run = 0.0f;
+
+  auto tile = [&](int j, auto MASK) {
+    const int kv0 = j * 64;
+    const char* kt = smem + (j & 1) * C::STAGE;
+    const char* vt = kt + C::KBYTES;
+    f32x16 s[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int kk = 0; kk < C::KSTEPS; ++kk) {
+      const int kc = 2 * kk + (lane >> 5);
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        const bf16x8 af = *(const bf16x8*)(kt + rm_addr<DH>(32 * mt + (lane & 31), kc));
+        s[mt] = mfma32x32x16(af, qf[kk], s[mt]);
+      }
+    }
+    if constexpr (decltype(MASK)::value) {
+      // key offset inside the tile of register r is 32*mt + 8*(r/4) + (r%4) + 4*(lane/32)
+      const int lim = kv_last - kv0 - 4 * (lane >> 5);
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          s[mt][r] = (32 * mt + 8 * (r >> 2) + (r & 3) <= lim) ? s[mt][r] : NEG_INF;
+    }
+    float mx = NEG_INF;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
+    mx = max_halves(mx);
+    const bool up = (mx - m_run) * c > RESCALE_LOG2;      // true on the first visible tile
+    if (__ballot(up)) {
+      asm volatile("" ::: "memory");                       // keep the rescale behind the branch
+      const float corr = up ? fast_exp2((m_run - mx) * c) : 1.0f;   // exp2(-inf) = 0
+      l_run *= corr;
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t) acc[t] *= corr;
+    }
+    if (up) m_run = mx;
+    const float mc = (m_run == NEG_INF ? 0.0f : m_run) * c;
+    float rs = 0.0f;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(fmaf(s[mt][r], c, -mc));
+        s[mt][r] = p;
+        rs += p;
+      }
+    l_run += rs;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const bf16x8 pb = acc_to_b(s[mt], hf);
+#pragma unroll
+        for (int t = 0; t < C::DT; ++t) {
+          const bf16x8 af = fm_frag<DH>(vt, 32 * t + (lane & 31), 32 * mt + 16 * hf, lane);
+          acc[t] = mfma32x32x16(af, pb, acc[t]);
+        }
+      }
+  };
+
+  // Key tiles every query of the workgroup fully sees come first (unmasked body);
+  // the diagonal and ragged tiles follow (masked body). Both loops are uniform over
+  // the workgroup, so every barrier is reached by all waves.
+  int n_full = a.causal ? std::min(ntiles, (q0 + 1) / 64) : ntiles;
+  n_full = std::min(n_full, S / 64);
+  if (ntiles > 0) issue(0);
+  wait_dma();
+  __syncthreads();
+  int j = 0;
+  for (; j < n_full; ++j) {
+    if (j + 1 < ntiles) issue(j + 1);
+    tile(j, std::false_type{});
+    wait_dma();
+    __syncthreads();
+  }
+  for (; j < ntiles; ++j) {
+    if (j + 1 < ntiles) issue(j + 1);
+    if (!(a.causal && j * 64 > qw + 31)) tile(j, std::true_type{});
+    wait_dma();
+    __syncthreads();
+  }
+
+  const float l_tot = sum_halves(l_run);
+  if (qrow < (int)a.q_end && qrow < S) {
+    const float inv = 1.0f / l_tot;
+    bf16* Op = (bf16*)a.o + ((int64_t)b * a.S + qrow) * a.ld_o + h * DH;
+#pragma unroll
+    for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        bf16x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = (bf16)(acc[t][4 * rg + e] * inv);
+        *(bf16x4*)(Op + 32 * t + 8 * rg + 4 * (lane >> 5)) = v;
+      }
+    if (lane < 32) a.lse[((int64_t)b * a.H + h) * a.Sp + qrow] = m_run * scale + logf(l_tot);
+  }
+}
+
+// ====================================================================== fp32 kernels
+template <int DH>
+__global__ __launch_bounds__(64) void attn_fwd_f32_kernel(AttnArgs a) {
+  __shared__ float Ks[32][DH + 1], Vs[32][DH + 1];
+  const int tid = threadIdx.x, h = blockIdx.y, b = a.b_begin + blockIdx.z;
+  const int64_t S = a.S;
+  const int64_t q0 = a.q_begin + (int64_t)blockIdx.x * 64, q = q0 + tid;
+  const float scale = rsqrtf((float)DH), c = scale * LOG2E;
+  const float* Qp = (const float*)a.q + (int64_t)h * DH;
+  const float* Kp = (const float*)a.k + (int64_t)h * DH;
+  const float* Vt = (const float*)a.vt + (int64_t)h * DH * a.ld_vt + (int64_t)b * a.Sp;
+  float qr[DH], acc[DH];
+#pragma unroll
+  for (int d = 0; d < DH; ++d) {
+    qr[d] = q < S ? Qp[(b * S + q) * a.ld_q + d] : 0.0f;
+    acc[d] = 0.0f;
+  }
+  float m_run = NEG_INF, l_run = 0.0f;
+  const int64_t kv_end = a.causal ? (q0 + 64 < S ? q0 + 64 : S) : S;
+  for (int64_t kv0 = 0; kv0 < kv_end; kv0 += 32) {
+    for (int i = tid; i < 32 * DH; i += 64) {
+      const int r = i / DH, d = i % DH;
+      const int64_t kv = kv0 + r;
+      Ks[r][d] = kv < S ? Kp[(b * S + kv) * a.ld_k + d] : 0.0f;
+      const int d2 = i / 32, r2 = i % 32;
+      Vs[r2][d2] = (kv0 + r2 < S) ? Vt[(int64_t)d2 * a.ld_vt + kv0 + r2] : 0.0f;
+    }
+    __syncthreads();
+    float sc[32];
+    float mx = NEG_INF;
+#pragma unroll
+    for (int jj = 0; jj < 32; ++jj) {
+      float sv = 0.0f;
+#pragma unroll
+      for (int d = 0; d < DH; ++d) sv = fmaf(qr[d], Ks[jj][d], sv);
+      const int64_t kv = kv0 + jj;
+      if (kv >= S || (a.causal && kv > q)) sv = NEG_INF;
+      sc[jj] = sv;
+      mx = fmaxf(mx, sv);
+    }
+    const float m_new = fmaxf(m_run, mx);
+    const float m_use = (m_new == NEG_INF) ? 0.0f : m_new;
+    const float corr = exp2f((m_run - m_use) * c);
+    l_run *= corr;
+#pragma unroll
+    for (int d = 0; d < DH; ++d) acc[d] *= corr;
+#pragma unroll
+    for (int jj = 0; jj < 32; ++jj) {
+      const float p = exp2f((sc[jj] - m_use) * c);
+      l_run += p;
+#pragma unroll
+      for (int d = 0; d < DH; ++d) acc[d] = fmaf(p, Vs[jj][d], acc[d]);
+    }
+    m_run = m_new;
+    __syncthreads();
+  }
+  if (q < a.q_end && q < S) {
+    float* Op = (float*)a.o + (b * S + q) * a.ld_o + (int64_t)h * DH;
+    const float inv = 1.0f / l_run;
+#pragma unroll
+    for (int d = 0; d < DH; ++d) Op[d] = acc[d] * inv;
+    a.lse[((int64_t)b * a.H + h) * a.Sp + q] = m_run * scale + logf(l_run);
+  }
+}
+
+
+template <int DH>
+static hipError_t fwd_launch(Dt dt, const AttnArgs& a, hipStream_t s) {
+  const int64_t nq = a.q_end - a.q_begin;
+  if (nq <= 0 || a.nb <= 0) return hipSuccess;
+  if (dt == BF16) {
+    auto kern = attn_fwd_bf16_kernel<DH>;
+    hipError_t e = set_lds(kern, FwdCfg<DH>::LDS);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)((nq + 127) / 128), a.H, a.nb), dim3(256),
+                       FwdCfg<DH>::LDS, s, a);
+  } else {
+    hipLaunchKernelGGL(attn_fwd_f32_kernel<DH>, dim3((unsigned)((nq + 63) / 64), a.H, a.nb),
+                       dim3(64), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t attn_fwd(Dt dt, const AttnArgs& a, hipStream_t s) {
+  if (a.dh == 64) return fwd_launch<64>(dt, a, s);
+  if (a.dh == 128) return fwd_launch<128>(dt, a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace bpt

@@ -53,6 +53,7 @@ struct AttnArgs {
   void* dqt = nullptr; void* dkt = nullptr; void* dvt = nullptr; int64_t ld_dt = 0;
   float* lse = nullptr;        // [B, H, Sp] natural log
   const float* delta = nullptr;// [B, H, Sp]
+  const float* lse2 = nullptr; // [B, H, Sp] log-sum-exp in base 2 (backward)
   int64_t S = 0, Sp = 0;
   int B = 0, H = 0, dh = 0;
   int causal = 0;
@@ -61,8 +62,9 @@ struct AttnArgs {
 };
 
 hipError_t attn_fwd(Dt dt, const AttnArgs& a, hipStream_t s);
-// part 0: dK and dV (key-outer kernel); part 1: dQ (query-outer kernel)
-hipError_t attn_bwd(Dt dt, int part, const AttnArgs& a, hipStream_t s);
+// backward: dK and dV (key-outer kernel), dQ (query-outer kernel)
+hipError_t attn_bwd_dkdv(Dt dt, const AttnArgs& a, hipStream_t s);
+hipError_t attn_bwd_dq(Dt dt, const AttnArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- row-wise / layout kernels
 // LayerNorm over D per row. x: [rows, D] (ti); out [rows, D] (to).
@@ -99,8 +101,9 @@ hipError_t col_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols,
 hipError_t row_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols, float* out,
                    int accumulate, hipStream_t s);
 
-// delta[b, h, s] = sum_d dO[b*S+s, h*dh+d] * O[b*S+s, h*dh+d]
-hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, float* delta, int B,
-                      int64_t S, int64_t Sp, int H, int dh, hipStream_t s);
+// delta[b, h, s] = sum_d dO[b*S+s, h*dh+d] * O[b*S+s, h*dh+d]; lse2 = lse * log2(e);
+// both are 0 for the padding positions s >= S
+hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, const float* lse, float* delta,
+                      float* lse2, int B, int64_t S, int64_t Sp, int H, int dh, hipStream_t s);
 
 }  // namespace bpt

@@ -12,7 +12,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/libbpt.h"
+#include "libbpt.h"
 #include "internal.h"
 
 using namespace bpt;
@@ -142,7 +142,7 @@ struct BwdWs {
   void *w1T, *wcat;
   void *vg, *vgT, *gT, *dzT, *dz, *dyT;
   float* gpT;
-  float *dv, *dh, *dU, *delta, *partial, *scratch;
+  float *dv, *dh, *dU, *delta, *lse2, *partial, *scratch;
   void *dhe, *dhT, *oT, *dO, *dOT, *V, *qT, *kT, *dqkvT, *dqkv, *u, *uT;
 };
 
@@ -166,6 +166,7 @@ BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
   w.dO = bp.take(d.T * d.D * d.E);
   w.dOT = bp.take(d.D * d.Tp * d.E);
   w.delta = (float*)bp.take(d.B * d.H * d.Sp * 4);
+  w.lse2 = (float*)bp.take(d.B * d.H * d.Sp * 4);
   w.V = bp.take(d.T * d.D * d.E);
   w.qT = bp.take(d.D * d.Tp * d.E);
   w.kT = bp.take(d.D * d.Tp * d.E);
@@ -564,7 +565,7 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
   }
 
   // ---- attention backward, probabilities rebuilt from the saved log-sum-exp
-  RUN("attn.delta", 0, 2.0 * T * D * E_, attn_delta(E, w.dO, sv.o, D, w.delta, B, S, Sp, (int)d.H, (int)d.dh, s));
+  RUN("attn.delta", 0, 2.0 * T * D * E_, attn_delta(E, w.dO, sv.o, D, sv.lse, w.delta, w.lse2, B, S, Sp, (int)d.H, (int)d.dh, s));
   RUN("transpose.act", 0, tb * T * D, transpose(E, sv.vt, Tp, Sp, w.V, D, S * D, D, S, D, B, s));
   RUN("transpose.act", 0, tb * T * D, transpose(E, sv.qk, 2 * D, S * 2 * D, w.qT, Tp, Sp, S, D, Sp, B, s));
   RUN("transpose.act", 0, tb * T * D, transpose(E, off(sv.qk, D * E_), 2 * D, S * 2 * D, w.kT, Tp, Sp, S, D, Sp, B, s));
@@ -579,13 +580,13 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     a.kt = w.kT; a.ld_kt = Tp;
     a.dot = w.dOT; a.ld_dot = Tp;
     a.dqt = w.dqkvT; a.dkt = off(w.dqkvT, D * Tp * E_); a.dvt = off(w.dqkvT, 2 * D * Tp * E_); a.ld_dt = Tp;
-    a.lse = sv.lse; a.delta = w.delta;
+    a.lse = sv.lse; a.delta = w.delta; a.lse2 = w.lse2;
     a.S = S; a.Sp = Sp; a.B = B; a.H = (int)d.H; a.dh = (int)d.dh; a.causal = cfg->causal;
     const double pairs = attn_pairs(0, S, S, cfg->causal) * d.H * B;
     // key-outer: S = Q K^T, dP = dO V^T, dV += P^T dO, dK += dS^T Q (4 contractions)
-    RUN("attn.bwd_dkdv", 8.0 * d.dh * pairs, 8.0 * T * D * E_, attn_bwd(E, 0, a, s));
+    RUN("attn.bwd_dkdv", 8.0 * d.dh * pairs, 8.0 * T * D * E_, attn_bwd_dkdv(E, a, s));
     // query-outer: S^T, dP^T, dQ += dS K (3 contractions)
-    RUN("attn.bwd_dq", 6.0 * d.dh * pairs, 6.0 * T * D * E_, attn_bwd(E, 1, a, s));
+    RUN("attn.bwd_dq", 6.0 * d.dh * pairs, 6.0 * T * D * E_, attn_bwd_dq(E, a, s));
   }
 
   // ---- QKV projection and LN1 backward

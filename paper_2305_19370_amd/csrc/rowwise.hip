@@ -182,8 +182,9 @@ __global__ __launch_bounds__(256) void row_sum_kernel(const T* in, int64_t ld, i
 
 // ------------------------------------------------------------------ softmax-backward Delta
 template <typename T>
-__global__ __launch_bounds__(256) void delta_kernel(const T* dO, const T* O, int64_t ld, float* delta,
-                                                    int B, int64_t S, int64_t Sp, int H, int dh) {
+__global__ __launch_bounds__(256) void delta_kernel(const T* dO, const T* O, int64_t ld, const float* lse,
+                                                    float* delta, float* lse2, int B, int64_t S, int64_t Sp,
+                                                    int H, int dh) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;     // over B * H * Sp
   if (i >= (int64_t)B * H * Sp) return;
   const int64_t s = i % Sp;
@@ -200,6 +201,7 @@ __global__ __launch_bounds__(256) void delta_kernel(const T* dO, const T* O, int
     }
   }
   delta[i] = acc;
+  lse2[i] = s < S ? lse[i] * 1.4426950408889634f : 0.0f;
 }
 
 // ------------------------------------------------------------------ transpose / copy
@@ -302,11 +304,11 @@ hipError_t row_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols,
   return hipGetLastError();
 }
 
-hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, float* delta, int B, int64_t S,
-                      int64_t Sp, int H, int dh, hipStream_t s) {
+hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, const float* lse, float* delta,
+                      float* lse2, int B, int64_t S, int64_t Sp, int H, int dh, hipStream_t s) {
   const int64_t n = (int64_t)B * H * Sp;
   BPT_T(t, T, hipLaunchKernelGGL((delta_kernel<T>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                                 (const T*)dout, (const T*)o, ld, delta, B, S, Sp, H, dh));
+                                 (const T*)dout, (const T*)o, ld, lse, delta, lse2, B, S, Sp, H, dh));
   return hipGetLastError();
 }
 
