@@ -99,70 +99,99 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
 }
 
 // ------------------------------------------------------------------ bf16 MFMA kernel
+// Tile BM x BN (2 x 2 waves), K step 32 per stage, NS stages in an LDS ring filled
+// by direct global->LDS copies (global_load_lds_dwordx4) issued NS-1 stages ahead.
+// Tile rows are 32 bf16 (64 bytes) padded to 80 bytes, so the 16 rows of a
+// fragment read fall in distinct bank groups and every fragment address is a
+// per-lane base plus an immediate. K must be a multiple of 32 (host-checked).
 template <int BM, int BN>
 struct TileCfg {
-  static constexpr int BK = 64;
+  static constexpr int BK = 32;
+  static constexpr int PITCH = 80, SLOTS = 5;          // bytes / 16-byte slots per tile row
   static constexpr int WM = BM / 2, WN = BN / 2;      // wave tile (2 x 2 waves)
   static constexpr int TM = WM / 32, TN = WN / 32;    // 32x32 MFMA tiles per wave
-  static constexpr int CA = BM * 8 / 256, CB = BN * 8 / 256;   // 16-byte chunks per thread
-  static constexpr int LDS = 2 * (BM + BN) * BK * 2;  // bytes, double buffered
+  static constexpr int ABYTES = BM * PITCH, BBYTES = BN * PITCH;
+  static constexpr int ABLK = ABYTES / 1024, BBLK = BBYTES / 1024;    // 1 KB copy blocks
+  static constexpr int APW = (ABLK + 3) / 4, BPW = (BBLK + 3) / 4;    // copies per wave
+  static constexpr int DPS = APW + BPW;               // copy instructions per wave per stage
+  static constexpr int STAGE = ABYTES + BBYTES;
+  static constexpr int NS = 4;                        // stages in the ring
+  static constexpr int LDS = NS * STAGE;
+  static_assert(ABYTES % 1024 == 0 && BBYTES % 1024 == 0, "whole copy blocks");
+  static_assert(4 * (WN + 4) * 32 * 4 <= LDS, "epilogue staging fits");
 };
 
-// 16-byte chunk `kc` (8 bf16 along K) of tile row `row`, XOR-swizzled by row.
-BPT_DEV int swz(int row, int kc) { return row * 128 + ((kc ^ (row & 7)) << 4); }
-
-BPT_DEV u32x4 load_chunk_bf16(const bf16* rowp, int64_t k, int64_t K) {
-  if (k + 8 <= K) return *(const u32x4*)(rowp + k);
-  union { u32x4 v; uint16_t h[8]; } u;
-  const uint16_t* p = (const uint16_t*)rowp;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) u.h[e] = (k + e < K) ? p[k + e] : (uint16_t)0;
-  return u.v;
+// One wave copies 1 KiB from global memory straight into LDS: lane l's 16 bytes land at
+// lds_block + 16 l. Written as inline assembly on purpose: the compiler's counter
+// tracking treats the builtin form as a pending FLAT access and then turns every later
+// LDS-fragment wait into a full drain. Completion is tracked by hand (wait_vmcnt). M0 is
+// a reserved register the compiler does not otherwise use in these kernels.
+BPT_DEV void lds_dma16(const void* g, char* lds_block) {
+  const uint32_t m = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_block);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(g), "s"(m) : "memory");
 }
+
+template <int N> BPT_DEV void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
 template <int BM, int BN, int EPI, typename CT, typename RT>
 __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
   using Cfg = TileCfg<BM, BN>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  const int64_t tiles_m = (a.M + BM - 1) / BM;
-  const int64_t tm = blockIdx.x % tiles_m, tn = blockIdx.x / tiles_m;
-  const int64_t m0 = tm * BM, n0 = tn * BN, z = blockIdx.z;
-  const bf16* A = (const bf16*)a.A + z * a.sA;
-  const bf16* B = (const bf16*)a.B + z * a.sB;
-  const int64_t K = a.K;
-  const int nk = (int)((K + Cfg::BK - 1) / Cfg::BK);
+  // Grouped tile order: 8 consecutive workgroups (one per XCD) take 8 row blocks of
+  // the same column block; each XCD thus keeps one row block of A in its L2.
+  const int tiles_m = (int)((a.M + BM - 1) / BM);
+  const int64_t ncols = a.Nstore > a.N ? a.Nstore : a.N;
+  const int tiles_n = (int)((ncols + BN - 1) / BN);
+  constexpr int GM = 8;
+  const int pid = blockIdx.x;
+  const int group = pid / (GM * tiles_n), first_m = group * GM;
+  const int gm = tiles_m - first_m < GM ? tiles_m - first_m : GM;
+  const int tm = first_m + (pid % (GM * tiles_n)) % gm;
+  const int tn = (pid % (GM * tiles_n)) / gm;
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN, z = blockIdx.z;
+  const bf16* A = (const bf16*)a.A + z * a.sA + m0 * a.lda;
+  const bf16* B = (const bf16*)a.B + z * a.sB + n0 * a.ldb;
+  const int nk = (int)(a.K / Cfg::BK);
 
-  // stage `buf` holds the A tile (BM rows of 128 bytes) followed by the B tile
-  auto As = [&](int buf) { return smem + buf * (BM + BN) * 128; };
-  auto Bs = [&](int buf) { return smem + buf * (BM + BN) * 128 + BM * 128; };
-
-  u32x4 ra[Cfg::CA], rb[Cfg::CB];
-  auto gload = [&](int kt) {
+  // per-lane source offsets (elements) of this wave's copy slots; rows past the
+  // matrix edge are clamped to its last row (their results are never stored)
+  int aoff[Cfg::APW], boff[Cfg::BPW];
+  {
+    const int alast = (int)(a.M - 1 - m0), blast = (int)(a.N - 1 - n0);
 #pragma unroll
-    for (int i = 0; i < Cfg::CA; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-      const int64_t m = m0 + row;
-      ra[i] = (m < a.M) ? load_chunk_bf16(A + m * a.lda, (int64_t)kt * 64 + kc * 8, K) : u32x4{0, 0, 0, 0};
+    for (int i = 0; i < Cfg::APW; ++i) {
+      int blk = wave + 4 * i;
+      blk = blk < Cfg::ABLK ? blk : Cfg::ABLK - 1;     // extra copies repeat the last block
+      const int slot = blk * 64 + lane, row = slot / Cfg::SLOTS, col = slot % Cfg::SLOTS;
+      aoff[i] = (row < alast ? row : alast) * (int)a.lda + (col < 4 ? col : 0) * 8;
     }
 #pragma unroll
-    for (int i = 0; i < Cfg::CB; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-      const int64_t n = n0 + row;
-      rb[i] = (n < a.N) ? load_chunk_bf16(B + n * a.ldb, (int64_t)kt * 64 + kc * 8, K) : u32x4{0, 0, 0, 0};
+    for (int i = 0; i < Cfg::BPW; ++i) {
+      int blk = wave + 4 * i;
+      blk = blk < Cfg::BBLK ? blk : Cfg::BBLK - 1;
+      const int slot = blk * 64 + lane, row = slot / Cfg::SLOTS, col = slot % Cfg::SLOTS;
+      boff[i] = (row < blast ? row : blast) * (int)a.ldb + (col < 4 ? col : 0) * 8;
     }
-  };
-  auto lstore = [&](int buf) {
+  }
+  auto issue = [&](int kt) {
+    char* st = smem + (kt % Cfg::NS) * Cfg::STAGE;
+    const int k0 = kt * Cfg::BK;
 #pragma unroll
-    for (int i = 0; i < Cfg::CA; ++i) {
-      const int c = tid + 256 * i;
-      *(u32x4*)(As(buf) + swz(c >> 3, c & 7)) = ra[i];
+    for (int i = 0; i < Cfg::APW; ++i) {
+      int blk = wave + 4 * i;
+      blk = blk < Cfg::ABLK ? blk : Cfg::ABLK - 1;
+      lds_dma16(A + k0 + aoff[i], st + blk * 1024);
     }
 #pragma unroll
-    for (int i = 0; i < Cfg::CB; ++i) {
-      const int c = tid + 256 * i;
-      *(u32x4*)(Bs(buf) + swz(c >> 3, c & 7)) = rb[i];
+    for (int i = 0; i < Cfg::BPW; ++i) {
+      int blk = wave + 4 * i;
+      blk = blk < Cfg::BBLK ? blk : Cfg::BBLK - 1;
+      lds_dma16(B + k0 + boff[i], st + Cfg::ABYTES + blk * 1024);
     }
   };
 
@@ -172,46 +201,73 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < Cfg::TN; ++j) acc[i][j] = f32x16{};
 
+  const int abase = (wm * Cfg::WM + (lane & 31)) * Cfg::PITCH + (lane >> 5) * 16;
+  const int bbase = Cfg::ABYTES + (wn * Cfg::WN + (lane & 31)) * Cfg::PITCH + (lane >> 5) * 16;
+
+  // Fragments are double-buffered in registers: the LDS reads of the next k step are
+  // issued before the MFMAs of the current one, so their latency hides behind them.
+  bf16x8 fa[2][Cfg::TM], fb[2][Cfg::TN];
+  auto load_frags = [&](int kt, int kk, int buf) {
+    const char* st = smem + (kt % Cfg::NS) * Cfg::STAGE;
+#pragma unroll
+    for (int i = 0; i < Cfg::TM; ++i) fa[buf][i] = *(const bf16x8*)(st + abase + i * 32 * Cfg::PITCH + kk * 32);
+#pragma unroll
+    for (int j = 0; j < Cfg::TN; ++j) fb[buf][j] = *(const bf16x8*)(st + bbase + j * 32 * Cfg::PITCH + kk * 32);
+  };
+  auto mfmas = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < Cfg::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < Cfg::TN; ++j) acc[i][j] = mfma32x32x16(fa[buf][i], fb[buf][j], acc[i][j]);
+  };
+
+  // stages 0 .. NS-2 in flight; wait for stage 0
+#pragma unroll
+  for (int s = 0; s < Cfg::NS - 1; ++s)
+    if (s < nk) issue(s);
+  if (nk >= Cfg::NS - 1) wait_vmcnt<(Cfg::NS - 2) * Cfg::DPS>();
+  else wait_vmcnt<0>();
+  __syncthreads();
+  if (nk > 0) load_frags(0, 0, 0);
+  // steady state, branch-free in the LDS reads so that each MFMA group waits only for
+  // its own fragments; the last stage is peeled below
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    load_frags(kt, 1, 1);                       // second k step of this stage
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas(0);
+    __builtin_amdgcn_sched_barrier(0);
+    // the slot of stage kt-1 is free: every wave finished reading it before the
+    // previous barrier
+    if (kt + Cfg::NS - 1 < nk) issue(kt + Cfg::NS - 1);
+    // stage kt+1 has landed once at most the stages issued after it are pending
+    if (kt + Cfg::NS - 1 < nk) wait_vmcnt<(Cfg::NS - 2) * Cfg::DPS>();
+    else if (kt + Cfg::NS - 2 < nk) wait_vmcnt<(Cfg::NS - 3) * Cfg::DPS>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    load_frags(kt + 1, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas(1);
+    __builtin_amdgcn_sched_barrier(0);
+  }
   if (nk > 0) {
-    gload(0);
-    lstore(0);
+    load_frags(nk - 1, 1, 1);
+    mfmas(0);
+    mfmas(1);
   }
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int kc = kk * 2 + (lane >> 5);
-      bf16x8 af[Cfg::TM], bfr[Cfg::TN];
-#pragma unroll
-      for (int i = 0; i < Cfg::TM; ++i)
-        af[i] = *(const bf16x8*)(As(buf) + swz(wm * Cfg::WM + 32 * i + (lane & 31), kc));
-#pragma unroll
-      for (int j = 0; j < Cfg::TN; ++j)
-        bfr[j] = *(const bf16x8*)(Bs(buf) + swz(wn * Cfg::WN + 32 * j + (lane & 31), kc));
-#pragma unroll
-      for (int i = 0; i < Cfg::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < Cfg::TN; ++j) acc[i][j] = mfma32x32x16(af[i], bfr[j], acc[i][j]);
-    }
-    if (kt + 1 < nk) lstore(buf ^ 1);
-    __syncthreads();
-  }
 
   // Epilogue: each wave stages one 32-row strip of its accumulators in LDS (free
   // after the K loop), then every lane applies the epilogue to groups of 4
   // consecutive columns and stores them with one vector store.
-  const int64_t ncols = a.Nstore > a.N ? a.Nstore : a.N;
-  constexpr int PITCH = Cfg::WN + 4;                 // floats per staged row
-  float* strip = (float*)smem + wave * 32 * PITCH;
+  constexpr int PITCHF = Cfg::WN + 4;                // floats per staged row
+  float* strip = (float*)smem + wave * 32 * PITCHF;
 #pragma unroll
   for (int i = 0; i < Cfg::TM; ++i) {
 #pragma unroll
     for (int j = 0; j < Cfg::TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        strip[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * PITCH + 32 * j + (lane & 31)] = acc[i][j][r];
+        strip[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * PITCHF + 32 * j + (lane & 31)] = acc[i][j][r];
     __syncthreads();
 #pragma unroll 1
     for (int e = lane; e < 32 * Cfg::WN / 4; e += 64) {
@@ -219,7 +275,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
       const int64_t m = m0 + wm * Cfg::WM + 32 * i + row;
       const int64_t n = n0 + wn * Cfg::WN + 4 * c4;
       if (m < a.M && n < ncols) {
-        const f32x4 v = *(const f32x4*)(strip + row * PITCH + 4 * c4);
+        const f32x4 v = *(const f32x4*)(strip + row * PITCHF + 4 * c4);
         epi_store4<EPI, CT, RT>(a, z, m, n, ncols, v);
       }
     }
@@ -285,6 +341,7 @@ static hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
   const int64_t ncols = a.Nstore > a.N ? a.Nstore : a.N;
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((ncols + BN - 1) / BN);
   if (tiles <= 0 || a.batch <= 0) return hipSuccess;
+  if (a.K % Cfg::BK != 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL(kern, dim3((unsigned)tiles, 1, (unsigned)a.batch), dim3(256), Cfg::LDS, s, a);
   return hipGetLastError();
 }
