@@ -12,6 +12,7 @@
 // banks. fp32 path: plain VALU FMA tiles (used for the fp32 parity workload).
 #include "common.h"
 #include "internal.h"
+#include <type_traits>
 
 namespace bpt {
 
@@ -101,13 +102,15 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
 // ------------------------------------------------------------------ bf16 MFMA kernel
 // Tile BM x BN (2 x 2 waves), K step 32 per stage, NS stages in an LDS ring filled
 // by direct global->LDS copies (global_load_lds_dwordx4) issued NS-1 stages ahead.
-// Tile rows are 32 bf16 (64 bytes) padded to 80 bytes, so the 16 rows of a
-// fragment read fall in distinct bank groups and every fragment address is a
-// per-lane base plus an immediate. K must be a multiple of 32 (host-checked).
+// Tile rows are 32 bf16 (64 bytes, four 16-byte chunks) stored unpadded; chunk c of
+// row r sits at chunk position c ^ swz(r), which spreads the rows that one fragment read
+// touches over distinct bank groups. The copies apply the same permutation on the
+// global side, so a wave's 1 KiB copy block still lands contiguously. K must be a
+// multiple of 32 (host-checked).
 template <int BM, int BN>
 struct TileCfg {
   static constexpr int BK = 32;
-  static constexpr int PITCH = 80, SLOTS = 5;          // bytes / 16-byte slots per tile row
+  static constexpr int PITCH = 64;                     // bytes per tile row
   static constexpr int WM = BM / 2, WN = BN / 2;      // wave tile (2 x 2 waves)
   static constexpr int TM = WM / 32, TN = WN / 32;    // 32x32 MFMA tiles per wave
   static constexpr int ABYTES = BM * PITCH, BBYTES = BN * PITCH;
@@ -126,12 +129,15 @@ struct TileCfg {
 // tracking treats the builtin form as a pending FLAT access and then turns every later
 // LDS-fragment wait into a full drain. Completion is tracked by hand (wait_vmcnt). M0 is
 // a reserved register the compiler does not otherwise use in these kernels.
-BPT_DEV void lds_dma16(const void* g, char* lds_block) {
-  const uint32_t m = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_block);
+BPT_DEV void lds_dma16(const void* g, uint32_t lds_block) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(g), "s"(m) : "memory");
+               :: "v"(g), "s"(lds_block) : "memory");
 }
+
+// chunk permutation of tile row r: bits (r1 ^ r3, r2). Within any 8 consecutive rows,
+// and within any 16 consecutive rows of equal r mod 4, (row, chunk) pairs of one chunk
+// column fall in distinct 16-byte bank groups.
+BPT_DEV int swz(int r) { return (((r >> 1) ^ (r >> 3)) & 1) | (r & 4) >> 1; }
 
 template <int N> BPT_DEV void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
@@ -142,13 +148,19 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  // Grouped tile order: 8 consecutive workgroups (one per XCD) take 8 row blocks of
-  // the same column block; each XCD thus keeps one row block of A in its L2.
+  // Tile order. Workgroup i runs on XCD i % 8, and each XCD has its own L2. The ids are
+  // renumbered so that every XCD owns a contiguous range of tiles; within the range,
+  // tiles go down GM row blocks before moving to the next column block, so the ~32
+  // workgroups an XCD runs at once share 8 row blocks of A and ~4 column blocks of B.
   const int tiles_m = (int)((a.M + BM - 1) / BM);
   const int64_t ncols = a.Nstore > a.N ? a.Nstore : a.N;
   const int tiles_n = (int)((ncols + BN - 1) / BN);
-  constexpr int GM = 8;
-  const int pid = blockIdx.x;
+  constexpr int GM = 8, NXCD = 8;
+  int pid = blockIdx.x;
+  {
+    const int ntiles = tiles_m * tiles_n, q = ntiles / NXCD, r = ntiles % NXCD, x = pid % NXCD;
+    pid = x * q + (x < r ? x : r) + pid / NXCD;
+  }
   const int group = pid / (GM * tiles_n), first_m = group * GM;
   const int gm = tiles_m - first_m < GM ? tiles_m - first_m : GM;
   const int tm = first_m + (pid % (GM * tiles_n)) % gm;
@@ -167,31 +179,32 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
     for (int i = 0; i < Cfg::APW; ++i) {
       int blk = wave + 4 * i;
       blk = blk < Cfg::ABLK ? blk : Cfg::ABLK - 1;     // extra copies repeat the last block
-      const int slot = blk * 64 + lane, row = slot / Cfg::SLOTS, col = slot % Cfg::SLOTS;
-      aoff[i] = (row < alast ? row : alast) * (int)a.lda + (col < 4 ? col : 0) * 8;
+      const int slot = blk * 64 + lane, row = slot >> 2, col = (slot & 3) ^ swz(row);
+      aoff[i] = (row < alast ? row : alast) * (int)a.lda + col * 8;
     }
 #pragma unroll
     for (int i = 0; i < Cfg::BPW; ++i) {
       int blk = wave + 4 * i;
       blk = blk < Cfg::BBLK ? blk : Cfg::BBLK - 1;
-      const int slot = blk * 64 + lane, row = slot / Cfg::SLOTS, col = slot % Cfg::SLOTS;
-      boff[i] = (row < blast ? row : blast) * (int)a.ldb + (col < 4 ? col : 0) * 8;
+      const int slot = blk * 64 + lane, row = slot >> 2, col = (slot & 3) ^ swz(row);
+      boff[i] = (row < blast ? row : blast) * (int)a.ldb + col * 8;
     }
   }
-  auto issue = [&](int kt) {
-    char* st = smem + (kt % Cfg::NS) * Cfg::STAGE;
+  // copy d (0 <= d < DPS) of this wave for stage kt: A blocks first, then B blocks
+  // LDS address of the tile ring (the copies take LDS addresses, not generic pointers)
+  const uint32_t ring = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem);
+  auto dma = [&](int kt, int d) {
+    const uint32_t st = ring + (kt % Cfg::NS) * Cfg::STAGE;
     const int k0 = kt * Cfg::BK;
-#pragma unroll
-    for (int i = 0; i < Cfg::APW; ++i) {
-      int blk = wave + 4 * i;
+    if (d < Cfg::APW) {
+      int blk = wave + 4 * d;
       blk = blk < Cfg::ABLK ? blk : Cfg::ABLK - 1;
-      lds_dma16(A + k0 + aoff[i], st + blk * 1024);
-    }
-#pragma unroll
-    for (int i = 0; i < Cfg::BPW; ++i) {
-      int blk = wave + 4 * i;
+      lds_dma16(A + k0 + aoff[d], st + blk * 1024);
+    } else {
+      int blk = wave + 4 * (d - Cfg::APW);
       blk = blk < Cfg::BBLK ? blk : Cfg::BBLK - 1;
-      lds_dma16(B + k0 + boff[i], st + Cfg::ABYTES + blk * 1024);
+      lds_dma16(B + k0 + boff[d - Cfg::APW], st + Cfg::ABYTES + blk * 1024);
     }
   };
 
@@ -201,58 +214,83 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < Cfg::TN; ++j) acc[i][j] = f32x16{};
 
-  const int abase = (wm * Cfg::WM + (lane & 31)) * Cfg::PITCH + (lane >> 5) * 16;
-  const int bbase = Cfg::ABYTES + (wn * Cfg::WN + (lane & 31)) * Cfg::PITCH + (lane >> 5) * 16;
+  // per-lane fragment bases of the two k steps of a stage (row bits 1..3 come from the lane)
+  const int sw = swz(lane & 31), h = lane >> 5;
+  const int abase[2] = {(wm * Cfg::WM + (lane & 31)) * Cfg::PITCH + 16 * (h ^ sw),
+                        (wm * Cfg::WM + (lane & 31)) * Cfg::PITCH + 16 * ((2 + h) ^ sw)};
+  const int bbase[2] = {Cfg::ABYTES + (wn * Cfg::WN + (lane & 31)) * Cfg::PITCH + 16 * (h ^ sw),
+                        Cfg::ABYTES + (wn * Cfg::WN + (lane & 31)) * Cfg::PITCH + 16 * ((2 + h) ^ sw)};
 
-  // Fragments are double-buffered in registers: the LDS reads of the next k step are
-  // issued before the MFMAs of the current one, so their latency hides behind them.
+  // Fragments are double-buffered in registers. Fragment r of a k step (0: A0,
+  // 1..TN: B0.., then A1..) is read in the order the MFMAs of the next k step use them.
   bf16x8 fa[2][Cfg::TM], fb[2][Cfg::TN];
-  auto load_frags = [&](int kt, int kk, int buf) {
-    const char* st = smem + (kt % Cfg::NS) * Cfg::STAGE;
-#pragma unroll
-    for (int i = 0; i < Cfg::TM; ++i) fa[buf][i] = *(const bf16x8*)(st + abase + i * 32 * Cfg::PITCH + kk * 32);
-#pragma unroll
-    for (int j = 0; j < Cfg::TN; ++j) fb[buf][j] = *(const bf16x8*)(st + bbase + j * 32 * Cfg::PITCH + kk * 32);
+  auto read_frag = [&](const char* st, int kk, int buf, int r) {
+    if (r == 0) fa[buf][0] = *(const bf16x8*)(st + abase[kk]);
+    else if (r <= Cfg::TN) fb[buf][r - 1] = *(const bf16x8*)(st + bbase[kk] + (r - 1) * 32 * Cfg::PITCH);
+    else fa[buf][r - Cfg::TN] = *(const bf16x8*)(st + abase[kk] + (r - Cfg::TN) * 32 * Cfg::PITCH);
   };
-  auto mfmas = [&](int buf) {
+  // One k step: the TM x TN MFMAs on fragment buffer CUR, each followed by at most one
+  // fragment read of the next k step (stage rkt, half rkk) into the other buffer and by
+  // this wave's share of the copies of stage dkt, so that the LDS and copy traffic is
+  // spread over the MFMA stream instead of arriving in bursts.
+  auto kstep = [&](auto cur_c, auto read_c, auto dma_c, int rkt, int rkk, int dkt) {
+    constexpr int cur = decltype(cur_c)::value;
+    constexpr bool rd = decltype(read_c)::value, cp = decltype(dma_c)::value;
+    constexpr int TMN = Cfg::TM * Cfg::TN, NR = Cfg::TM + Cfg::TN;
+    const char* rst = smem + (rkt % Cfg::NS) * Cfg::STAGE;
 #pragma unroll
-    for (int i = 0; i < Cfg::TM; ++i)
+    for (int q = 0; q < TMN; ++q) {
+      acc[q / Cfg::TN][q % Cfg::TN] = mfma32x32x16(fa[cur][q / Cfg::TN], fb[cur][q % Cfg::TN],
+                                                    acc[q / Cfg::TN][q % Cfg::TN]);
+      if (rd && q < NR) read_frag(rst, rkk, 1 - cur, q);
+      if (cp) {
 #pragma unroll
-      for (int j = 0; j < Cfg::TN; ++j) acc[i][j] = mfma32x32x16(fa[buf][i], fb[buf][j], acc[i][j]);
+        for (int d = (q * Cfg::DPS + TMN - 1) / TMN; d < ((q + 1) * Cfg::DPS + TMN - 1) / TMN; ++d) dma(dkt, d);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
   };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using T_ = std::true_type;
+  using F_ = std::false_type;
 
   // stages 0 .. NS-2 in flight; wait for stage 0
 #pragma unroll
   for (int s = 0; s < Cfg::NS - 1; ++s)
-    if (s < nk) issue(s);
+    if (s < nk) {
+#pragma unroll
+      for (int d = 0; d < Cfg::DPS; ++d) dma(s, d);
+    }
   if (nk >= Cfg::NS - 1) wait_vmcnt<(Cfg::NS - 2) * Cfg::DPS>();
   else wait_vmcnt<0>();
   __syncthreads();
-  if (nk > 0) load_frags(0, 0, 0);
-  // steady state, branch-free in the LDS reads so that each MFMA group waits only for
-  // its own fragments; the last stage is peeled below
-  for (int kt = 0; kt + 1 < nk; ++kt) {
-    load_frags(kt, 1, 1);                       // second k step of this stage
-    __builtin_amdgcn_sched_barrier(0);
-    mfmas(0);
-    __builtin_amdgcn_sched_barrier(0);
-    // the slot of stage kt-1 is free: every wave finished reading it before the
-    // previous barrier
-    if (kt + Cfg::NS - 1 < nk) issue(kt + Cfg::NS - 1);
-    // stage kt+1 has landed once at most the stages issued after it are pending
-    if (kt + Cfg::NS - 1 < nk) wait_vmcnt<(Cfg::NS - 2) * Cfg::DPS>();
-    else if (kt + Cfg::NS - 2 < nk) wait_vmcnt<(Cfg::NS - 3) * Cfg::DPS>();
-    else wait_vmcnt<0>();
+  if (nk > 0) {
+#pragma unroll
+    for (int r = 0; r < Cfg::TM + Cfg::TN; ++r) read_frag(smem, 0, 0, r);
+  }
+  // Stage kt: the first k step reads the second half of stage kt and, while the ring
+  // still has stages to fetch, copies stage kt+NS-1 into the slot of stage kt-1 (every
+  // wave finished reading that slot before the previous barrier). The barrier then
+  // publishes stage kt+1, whose first half the second k step reads. The two loops differ
+  // only in whether copies remain; the last stage is peeled.
+  const int kcopy = nk - (Cfg::NS - 1) > 0 ? nk - (Cfg::NS - 1) : 0;
+  int kt = 0;
+  for (; kt < kcopy; ++kt) {
+    kstep(I0{}, T_{}, T_{}, kt, 1, kt + Cfg::NS - 1);
+    wait_vmcnt<(Cfg::NS - 2) * Cfg::DPS>();
     __syncthreads();
-    load_frags(kt + 1, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    mfmas(1);
-    __builtin_amdgcn_sched_barrier(0);
+    kstep(I1{}, T_{}, F_{}, kt + 1, 0, 0);
+  }
+  for (; kt + 1 < nk; ++kt) {
+    kstep(I0{}, T_{}, F_{}, kt, 1, 0);
+    wait_vmcnt<0>();
+    __syncthreads();
+    kstep(I1{}, T_{}, F_{}, kt + 1, 0, 0);
   }
   if (nk > 0) {
-    load_frags(nk - 1, 1, 1);
-    mfmas(0);
-    mfmas(1);
+    kstep(I0{}, T_{}, F_{}, nk - 1, 1, 0);
+    kstep(I1{}, F_{}, F_{}, 0, 0, 0);
   }
   __syncthreads();
 
