@@ -42,11 +42,19 @@ BPT_DEV u32x4 ld16(const void* p) { return *(const u32x4*)p; }
 
 // Direct global -> LDS copy: every lane of the wave fetches 16 bytes from its own
 // address; lane l's bytes land at lds_block + 16 * l (lds_block is wave-uniform).
+// Inline assembly rather than the builtin: the compiler's counter tracking treats the
+// builtin as a pending FLAT access and then drains every later LDS-read wait to zero.
+// Completion is waited for by hand (wait_dma); M0 is otherwise unused in these kernels.
+BPT_DEV uint32_t lds_addr(const char* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)p);
+}
 BPT_DEV void dma16(const void* g, char* lds_block) {
-  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds_block, 16, 0, 0);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(g), "s"(lds_addr(lds_block)) : "memory");
 }
 BPT_DEV void dma4(const void* g, char* lds_block) {
-  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds_block, 4, 0, 0);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+               :: "v"(g), "s"(lds_addr(lds_block)) : "memory");
 }
 BPT_DEV void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
