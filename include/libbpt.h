@@ -88,7 +88,9 @@ typedef struct {           /* fp32 device pointers, overwritten; NULL = not want
  * caller's `saved` buffer. E = element size of cfg->dtype; T = B*S tokens;
  * Sp = S rounded up to a multiple of 64.
  *   qk   [T, 2D] E   Q (unscaled) in columns [0, D), K in [D, 2D)
- *   vt   [D, B*Sp] E V transposed: V[b, s, f] at row f, column b*Sp + s; pad columns are 0
+ *   vt   [D, B*Sp] E V transposed: V[b, s, f] at row f, column b*Sp + s' where s' = s for
+ *                    fp32 and, for bf16, s with bits 2 and 3 swapped (a permutation inside
+ *                    each aligned group of 16 tokens); columns of tokens s >= S hold 0
  *   o    [T, D] E    attention output (heads concatenated), before Wo
  *   lse  [B, H, Sp] fp32  natural-log log-sum-exp of each query row's scores
  *   h    [T, D] fp32 residual stream after attention, X + O Wo

@@ -226,7 +226,9 @@ class Layer:
         return dX, grads
 
     def saved_views(self, saved: torch.Tensor) -> Dict[str, torch.Tensor]:
-        """Typed views of the saved activations (see bpt_saved_layout in include/libbpt.h)."""
+        """Typed views of the saved activations (see bpt_saved_layout in include/libbpt.h).
+
+        ``vt`` comes back in plain token order (for bf16 a permuted copy, not a view)."""
         c = self.cfg
         lay = saved_layout(c)
         E = _TORCH_DT[c.dtype]
@@ -238,9 +240,14 @@ class Layer:
             nbytes = n * (2 if dt == torch.bfloat16 else 4)
             return saved[off:off + nbytes].view(dt).view(*shape)
 
+        vt = view("vt", D * c.B * Sp, E, (D, c.B * Sp))
+        if c.dtype == BPT_BF16:
+            # undo the token permutation of the bf16 layout (bits 2 and 3 swapped)
+            t = torch.arange(c.B * Sp, device=vt.device)
+            vt = vt[:, (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1)]
         return {
             "qk": view("qk", T * 2 * D, E, (T, 2 * D)),
-            "vt": view("vt", D * c.B * Sp, E, (D, c.B * Sp)),
+            "vt": vt,
             "o": view("o", T * D, E, (T, D)),
             "lse": view("lse", c.B * c.H * Sp, torch.float32, (c.B, c.H, Sp)),
             "h": view("h", T * D, torch.float32, (T, D)),

@@ -139,17 +139,14 @@ BPT_DEV float sum_halves(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// A-operand fragment for a contraction over 16 tokens starting at `tok0` of a
-// feature-major LDS tile: lane l supplies row (row0 + l%32) at tokens
+// A-operand fragment for a contraction over 16 tokens starting at `tok0` (a multiple
+// of 16) of a feature-major LDS tile: lane l supplies row (row0 + l%32) at tokens
 // tok0 + 4*(l/32) + {0..3} and tok0 + 8 + 4*(l/32) + {0..3}, matching the order in
-// which an MFMA accumulator hands its rows to the next MFMA as a B operand.
+// which an MFMA accumulator hands its rows to the next MFMA as a B operand. The tile
+// holds its tokens in tok_perm order, which makes these 8 tokens one 16-byte chunk.
 template <int DH>
 BPT_DEV bf16x8 fm_frag(const char* tile, int row, int tok0, int lane) {
-  const char* p = tile + row * FmTile<DH>::PITCH + (tok0 + 4 * (lane >> 5)) * 2;
-  const u32x2 lo = *(const u32x2*)p;
-  const u32x2 hi = *(const u32x2*)(p + 16);
-  u32x4 v = {lo[0], lo[1], hi[0], hi[1]};
-  return __builtin_bit_cast(bf16x8, v);
+  return *(const bf16x8*)(tile + row * FmTile<DH>::PITCH + (tok0 + 8 * (lane >> 5)) * 2);
 }
 
 // Registers 8*hf .. 8*hf+7 of an accumulator as a bf16 B operand.

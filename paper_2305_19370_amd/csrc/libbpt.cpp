@@ -414,6 +414,7 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
     g.B = w.u; g.ldb = D; g.sB = d.S * D;
     g.C = sv.vt; g.ldc = d.Tp; g.sC = d.Sp;
     g.M = D; g.N = d.S; g.Nstore = d.Sp; g.K = D; g.batch = (int)d.B;
+    g.perm_cols = E == BF16;                      // attention operand token order
     RUN("gemm.vt", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
   }
 
@@ -566,10 +567,12 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
 
   // ---- attention backward, probabilities rebuilt from the saved log-sum-exp
   RUN("attn.delta", 0, 2.0 * T * D * E_, attn_delta(E, w.dO, sv.o, D, sv.lse, w.delta, w.lse2, B, S, Sp, (int)d.H, (int)d.dh, s));
-  RUN("transpose.act", 0, tb * T * D, transpose(E, sv.vt, Tp, Sp, w.V, D, S * D, D, S, D, B, s));
-  RUN("transpose.act", 0, tb * T * D, transpose(E, sv.qk, 2 * D, S * 2 * D, w.qT, Tp, Sp, S, D, Sp, B, s));
-  RUN("transpose.act", 0, tb * T * D, transpose(E, off(sv.qk, D * E_), 2 * D, S * 2 * D, w.kT, Tp, Sp, S, D, Sp, B, s));
-  RUN("transpose.act", 0, tb * T * D, transpose(E, w.dO, D, S * D, w.dOT, Tp, Sp, S, D, Sp, B, s));
+  // feature-major attention operands of the bf16 kernels use the permuted token order
+  const int tpo = E == BF16 ? TP_OUT : 0, tpi = E == BF16 ? TP_IN : 0;
+  RUN("transpose.act", 0, tb * T * D, transpose(E, sv.vt, Tp, Sp, w.V, D, S * D, D, S, D, B, s, tpi));
+  RUN("transpose.act", 0, tb * T * D, transpose(E, sv.qk, 2 * D, S * 2 * D, w.qT, Tp, Sp, S, D, Sp, B, s, tpo));
+  RUN("transpose.act", 0, tb * T * D, transpose(E, off(sv.qk, D * E_), 2 * D, S * 2 * D, w.kT, Tp, Sp, S, D, Sp, B, s, tpo));
+  RUN("transpose.act", 0, tb * T * D, transpose(E, w.dO, D, S * D, w.dOT, Tp, Sp, S, D, Sp, B, s, tpo));
   {
     AttnArgs a;
     a.q = sv.qk; a.ld_q = 2 * D;
