@@ -87,16 +87,13 @@ typedef struct {           /* fp32 device pointers, overwritten; NULL = not want
 /* Byte offsets of the tensors the forward saves for the backward, inside the
  * caller's `saved` buffer. E = element size of cfg->dtype; T = B*S tokens;
  * Sp = S rounded up to a multiple of 64.
- *   qk   [T, 2D] E   Q (unscaled) in columns [0, D), K in [D, 2D)
- *   vt   [D, B*Sp] E V transposed: V[b, s, f] at row f, column b*Sp + s' where s' = s for
- *                    fp32 and, for bf16, s with bits 2 and 3 swapped (a permutation inside
- *                    each aligned group of 16 tokens); columns of tokens s >= S hold 0
+ *   qkv  [T, 3D] E   Q (unscaled) in columns [0, D), K in [D, 2D), V in [2D, 3D)
  *   o    [T, D] E    attention output (heads concatenated), before Wo
  *   lse  [B, H, Sp] fp32  natural-log log-sum-exp of each query row's scores
  *   h    [T, D] fp32 residual stream after attention, X + O Wo
  *   mu1, rstd1, mu2, rstd2 [T] fp32  LayerNorm statistics                               */
 typedef struct {
-  size_t qk, vt, o, lse, h, mu1, rstd1, mu2, rstd2, total;
+  size_t qkv, o, lse, h, mu1, rstd1, mu2, rstd2, total;
 } bpt_saved_layout;
 
 /* Host-only checks of a configuration; never touches a GPU. */

@@ -32,7 +32,7 @@ class Config(ctypes.Structure):
 
 PARAM_FIELDS = ("ln1_g", "ln1_b", "Wq", "Wk", "Wv", "Wo", "ln2_g", "ln2_b", "W1", "b1", "W2", "b2")
 GRAD_FIELDS = ("dln1_g", "dln1_b", "dWq", "dWk", "dWv", "dWo", "dln2_g", "dln2_b", "dW1", "db1", "dW2", "db2")
-SAVED_FIELDS = ("qk", "vt", "o", "lse", "h", "mu1", "rstd1", "mu2", "rstd2", "total")
+SAVED_FIELDS = ("qkv", "o", "lse", "h", "mu1", "rstd1", "mu2", "rstd2", "total")
 
 
 class Params(ctypes.Structure):
@@ -226,13 +226,10 @@ class Layer:
         return dX, grads
 
     def saved_views(self, saved: torch.Tensor) -> Dict[str, torch.Tensor]:
-        """Typed views of the saved activations (see bpt_saved_layout in include/libbpt.h).
-
-        ``vt`` comes back in plain token order (for bf16 a permuted copy, not a view)."""
+        """Typed views of the saved activations (see bpt_saved_layout in include/libbpt.h)."""
         c = self.cfg
         lay = saved_layout(c)
         E = _TORCH_DT[c.dtype]
-        es = 2 if c.dtype == BPT_BF16 else 4
         T, D, Sp = c.B * c.S, c.D, (c.S + 63) // 64 * 64
 
         def view(name, n, dt, shape):
@@ -240,14 +237,8 @@ class Layer:
             nbytes = n * (2 if dt == torch.bfloat16 else 4)
             return saved[off:off + nbytes].view(dt).view(*shape)
 
-        vt = view("vt", D * c.B * Sp, E, (D, c.B * Sp))
-        if c.dtype == BPT_BF16:
-            # undo the token permutation of the bf16 layout (bits 2 and 3 swapped)
-            t = torch.arange(c.B * Sp, device=vt.device)
-            vt = vt[:, (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1)]
         return {
-            "qk": view("qk", T * 2 * D, E, (T, 2 * D)),
-            "vt": vt,
+            "qkv": view("qkv", T * 3 * D, E, (T, 3 * D)),
             "o": view("o", T * D, E, (T, D)),
             "lse": view("lse", c.B * c.H * Sp, torch.float32, (c.B, c.H, Sp)),
             "h": view("h", T * D, torch.float32, (T, D)),

@@ -6,15 +6,22 @@
 namespace bpt {
 
 // ====================================================================== backward dK dV, bf16
-// Key-outer: each wave owns 32 keys; loop over query tiles of 64 (two halves of
-// 32). S = Q K^T and dP = dO V^T have the key on the lane axis, so P and dS feed
-// dV^T += dO^T P and dK^T += Q^T dS directly as B operands.
+// Key-outer: each wave owns 64 keys (two blocks of 32) and loops over query tiles of
+// 64 (two halves of 32). S = Q K^T and dP = dO V^T have the key on the lane axis, so
+// P and dS feed dV^T += dO^T P and dK^T += Q^T dS directly as B operands; dO^T and
+// Q^T fragments come from the token-major tiles by transposing LDS reads. Every
+// fragment read from LDS feeds the MFMAs of both key blocks.
+// Query tiles are visited from the last one down, so all workgroups of a head start
+// on the same tiles (and share them in L2); the diagonal tiles come last.
 template <int DH>
 struct DkvCfg {
   static constexpr int KSTEPS = DH / 16, DT = DH / 32;
-  static constexpr int RBYTES = RmTile<DH>::BYTES, FBYTES = FmTile<DH>::BYTES;
-  static constexpr int STAGE = 2 * RBYTES + 2 * FBYTES + 2 * 64 * 4;   // Q, dO, Q^T, dO^T, lse, delta
-  static constexpr int LDS = 2 * STAGE;
+  static constexpr int KEYS = 256;                  // keys per workgroup (4 waves x 64)
+  static constexpr int TB = RmTile<DH>::BYTES;
+  static constexpr int STAGE = 2 * TB + 2 * 64 * 4; // Q, dO tiles; lse (base 2), delta
+  static constexpr int NS = 4;                      // stages in the ring
+  static constexpr int LDS = NS * STAGE;
+  static constexpr int DPS = Ring2<DH>::DPW + 2;    // copies per wave per stage
 };
 
 template <int DH>
@@ -23,11 +30,13 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int h = blockIdx.y, b = blockIdx.z;
   const int S = (int)a.S;
-  const int k0 = (int)blockIdx.x * 128;          // causal: low key tiles have the most queries
-  const int kw = k0 + 32 * wave;
-  const int kvrow = kw + (lane & 31);
+  const int nblk = (S + C::KEYS - 1) / C::KEYS;
+  int hh, blk;
+  xcd_map((int)blockIdx.x, nblk, a.H * a.B, hh, blk);
+  const int h = hh % a.H, b = hh / a.H;
+  const int k0 = blk * C::KEYS;                     // causal: low key blocks have the most queries
+  const int kw = k0 + 64 * wave;                    // first key of this wave
   const float scale = rsqrtf((float)DH);
   const float c = scale * LOG2E;
 
@@ -35,69 +44,72 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
   const bf16* Kb = (const bf16*)a.k + (int64_t)b * a.S * a.ld_k + h * DH;
   const bf16* Vb = (const bf16*)a.v + (int64_t)b * a.S * a.ld_v + h * DH;
   const bf16* dOb = (const bf16*)a.dout + (int64_t)b * a.S * a.ld_do + h * DH;
-  const bf16* Qtb = (const bf16*)a.qt + (int64_t)h * DH * a.ld_qt + (int64_t)b * a.Sp;
-  const bf16* dOtb = (const bf16*)a.dot + (int64_t)h * DH * a.ld_dot + (int64_t)b * a.Sp;
   const float* lse2 = a.lse2 + ((int64_t)b * a.H + h) * a.Sp;
   const float* delta = a.delta + ((int64_t)b * a.H + h) * a.Sp;
 
-  bf16x8 kf[C::KSTEPS], vf[C::KSTEPS];
-  {
-    const int kr = kvrow < S ? kvrow : S - 1;
+  bf16x8 kf[2][C::KSTEPS], vf[2][C::KSTEPS];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int key = kw + 32 * kb + (lane & 31), kr = key < S ? key : S - 1;
 #pragma unroll
     for (int kk = 0; kk < C::KSTEPS; ++kk) {
-      kf[kk] = __builtin_bit_cast(bf16x8, ld16(Kb + (int64_t)kr * a.ld_k + 16 * kk + 8 * (lane >> 5)));
-      vf[kk] = __builtin_bit_cast(bf16x8, ld16(Vb + (int64_t)kr * a.ld_v + 16 * kk + 8 * (lane >> 5)));
+      kf[kb][kk] = __builtin_bit_cast(bf16x8, ld16(Kb + (int64_t)kr * a.ld_k + 16 * kk + 8 * (lane >> 5)));
+      vf[kb][kk] = __builtin_bit_cast(bf16x8, ld16(Vb + (int64_t)kr * a.ld_v + 16 * kk + 8 * (lane >> 5)));
+      settle(kf[kb][kk]);
+      settle(vf[kb][kk]);
     }
   }
-  const bool kok = kvrow < S;
 
-  const int qstart = a.causal ? (k0 / 64) * 64 : 0;
+  const int qstart = a.causal ? k0 : 0;             // a multiple of 64
   const int ntiles = qstart < S ? (S - qstart + 63) / 64 : 0;
-  DmaPlan<RmTile<DH>::BLOCKS> pq, pdo;
-  DmaPlan<FmTile<DH>::BLOCKS> pqt;       // Q^T and dO^T share their leading dimension
-  plan_rows<DH>(pq, (int)a.ld_q, wave, lane);
-  plan_rows<DH>(pdo, (int)a.ld_do, wave, lane);
-  plan_cols<DH>(pqt, (int)a.ld_qt, wave, lane);
-  auto issue = [&](int j) {
-    const int qt0 = qstart + j * 64;
-    char* qs = smem + (j & 1) * C::STAGE;
-    dma_rows<DH>(qs, Qb, a.ld_q, qt0, S - 1, wave, lane, pq);
-    dma_rows<DH>(qs + C::RBYTES, dOb, a.ld_do, qt0, S - 1, wave, lane, pdo);
-    dma_cols<DH>(qs + 2 * C::RBYTES, Qtb, qt0, wave, pqt);
-    dma_cols<DH>(qs + 2 * C::RBYTES + C::FBYTES, dOtb, qt0, wave, pqt);
-    // base-2 lse, delta of the 64 queries (indices < Sp: in bounds; rows >= S are masked)
-    if (wave == 0) dma4(lse2 + qt0 + lane, qs + 2 * C::RBYTES + 2 * C::FBYTES);
-    if (wave == 1) dma4(delta + qt0 + lane, qs + 2 * C::RBYTES + 2 * C::FBYTES + 256);
+  const int n_diag = a.causal ? C::KEYS / 64 : 0;   // tiles jt < n_diag straddle the keys
+  // iteration it visits query tile jt = ntiles - 1 - it
+  auto issue = [&](int it) {
+    const int qt0 = qstart + 64 * (ntiles - 1 - it);
+    char* st = smem + (it % C::NS) * C::STAGE;
+    ring_issue<DH>(st, Qb, (int)a.ld_q, dOb, (int)a.ld_do, qt0, S - 1, wave, lane);
+    // base-2 lse and delta of the 64 queries (indices < Sp: in bounds; rows >= S are
+    // masked); every wave copies them, so that all waves count the same copies
+    dma4s(lse2 + qt0, 4u * lane, st + 2 * C::TB);
+    dma4s(delta + qt0, 4u * lane, st + 2 * C::TB + 256);
   };
 
-  f32x16 adv[C::DT], adk[C::DT];
+  f32x16 adv[2][C::DT], adk[2][C::DT];
 #pragma unroll
-  for (int t = 0; t < C::DT; ++t) {
-    mfma_agpr_zero(adv[t]);
-    mfma_agpr_zero(adk[t]);
-  }
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int t = 0; t < C::DT; ++t) {
+      mfma_agpr_zero(adv[kb][t]);
+      mfma_agpr_zero(adk[kb][t]);
+    }
 
-  auto tile = [&](int j, auto MASK) {
-    const int qt0 = qstart + j * 64;
-    const char* qs = smem + (j & 1) * C::STAGE;
-    const char* ds = qs + C::RBYTES;
-    const char* qts = ds + C::RBYTES;
-    const char* dts = qts + C::FBYTES;
-    const float* ls = (const float*)(dts + C::FBYTES);
-    // query offset inside the tile of register r: 32*mt + 8*(r/4) + (r%4) + 4*(lane/32);
-    // visible iff lo <= offset <= hi
-    const int lo = (a.causal ? kvrow - qt0 : 0) - 4 * (lane >> 5);
-    const int hi = (kok ? S - 1 - qt0 : -1) - 4 * (lane >> 5);
+  auto tile = [&](int it, auto MASK) {
+    const int qt0 = qstart + 64 * (ntiles - 1 - it);
+    const char* qs = smem + (it % C::NS) * C::STAGE;
+    const char* ds = qs + C::TB;
+    const float* ls = (const float*)(qs + 2 * C::TB);
+    // query offset inside the tile of register r: 32*mt + acc_row(r, lane); visible
+    // for key block kb iff lo[kb] <= offset <= hi[kb]
+    int lo[2], hi[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int key = kw + 32 * kb + (lane & 31);
+      lo[kb] = a.causal ? key - qt0 : 0;
+      hi[kb] = key < S ? S - 1 - qt0 : -1;
+    }
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      f32x16 s = f32x16{}, dp = f32x16{};
+      f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
 #pragma unroll
       for (int kk = 0; kk < C::KSTEPS; ++kk) {
-        const int kc = 2 * kk + (lane >> 5);
-        const bf16x8 aq = *(const bf16x8*)(qs + rm_addr<DH>(32 * mt + (lane & 31), kc));
-        s = mfma32x32x16(aq, kf[kk], s);
-        const bf16x8 ad = *(const bf16x8*)(ds + rm_addr<DH>(32 * mt + (lane & 31), kc));
-        dp = mfma32x32x16(ad, vf[kk], dp);
+        const bf16x8 aq = frag_rows<DH>(qs, 32 * mt, 2 * kk, lane);
+        const bf16x8 ad = frag_rows<DH>(ds, 32 * mt, 2 * kk, lane);
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          s[kb] = mfma32x32x16(aq, kf[kb][kk], s[kb]);
+          dp[kb] = mfma32x32x16(ad, vf[kb][kk], dp[kb]);
+        }
+        __builtin_amdgcn_sched_barrier(0);        // bound the fragments read ahead
       }
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
@@ -107,77 +119,91 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * rg + e;
-          float p = fast_exp2(fmaf(s[r], c, -l4[e]));
-          if constexpr (decltype(MASK)::value) {
-            const int off = 32 * mt + 8 * rg + e;
-            p = (off >= lo && off <= hi) ? p : 0.0f;
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb) {
+            float p = fast_exp2(fmaf(s[kb][r], c, -l4[e]));
+            if constexpr (decltype(MASK)::value) {
+              const int off = qi + e;
+              p = (off >= lo[kb] && off <= hi[kb]) ? p : 0.0f;
+            }
+            s[kb][r] = p;
+            dp[kb][r] = p * (dp[kb][r] - d4[e]);       // dS
           }
-          s[r] = p;
-          dp[r] = p * (dp[r] - d4[e]);           // dS
         }
+        __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        const bf16x8 pb = acc_to_b(s, hf);
-        const bf16x8 sb = acc_to_b(dp, hf);
+        const bf16x8 pb0 = acc_to_b(s[0], hf), pb1 = acc_to_b(s[1], hf);
+        const bf16x8 sb0 = acc_to_b(dp[0], hf), sb1 = acc_to_b(dp[1], hf);
 #pragma unroll
         for (int t = 0; t < C::DT; ++t) {
-          const bf16x8 ado = fm_frag<DH>(dts, 32 * t + (lane & 31), 32 * mt + 16 * hf, lane);
-          mfma_agpr(adv[t], ado, pb);
-          const bf16x8 aqt = fm_frag<DH>(qts, 32 * t + (lane & 31), 32 * mt + 16 * hf, lane);
-          mfma_agpr(adk[t], aqt, sb);
+          const bf16x8 ado = frag_tr<DH>(ds, 32 * mt + 16 * hf, 32 * t, lane);
+          mfma_agpr(adv[0][t], ado, pb0);
+          mfma_agpr(adv[1][t], ado, pb1);
+          const bf16x8 aqt = frag_tr<DH>(qs, 32 * mt + 16 * hf, 32 * t, lane);
+          mfma_agpr(adk[0][t], aqt, sb0);
+          mfma_agpr(adk[1][t], aqt, sb1);
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
     }
   };
 
-  // Phases (uniform over the workgroup, so every barrier is reached by all waves):
-  // query tiles that straddle this key tile's diagonal (masked), tiles that every
-  // key of the workgroup fully sees (unmasked), and a ragged tail (masked).
-  const int n_diag = a.causal ? std::min(ntiles, (k0 + 128 - qstart + 63) / 64) : 0;
-  const int n_full = (k0 + 128 <= S) ? std::max(n_diag, (S - qstart) / 64) : n_diag;
-  if (ntiles > 0) issue(0);
-  wait_dma();
-  __syncthreads();
-  int j = 0;
-  for (; j < n_diag; ++j) {
-    if (j + 1 < ntiles) issue(j + 1);
-    if (!(a.causal && qstart + j * 64 + 63 < kw)) tile(j, std::true_type{});
-    wait_dma();
-    __syncthreads();
+  // Phases, each a loop over one tile body (uniform over the workgroup, so every
+  // barrier is reached by all waves): the ragged last query tile (masked), the tiles
+  // every key of the workgroup fully sees (unmasked), and the tiles that straddle the
+  // workgroup's keys (masked); a wave skips the arithmetic of tiles entirely before
+  // its keys.
+  const bool ragged = ntiles > 0 && qstart + 64 * (ntiles - 1) + 63 >= S;
+  const int it_a = ragged ? 1 : 0;
+  const int it_b = k0 + C::KEYS > S ? it_a : std::max(it_a, ntiles - n_diag);
+  auto step = [&](int it) {
+    if (it + 2 < ntiles) wait_vmcnt<2 * C::DPS>();
+    else if (it + 1 < ntiles) wait_vmcnt<C::DPS>();
+    else wait_vmcnt<0>();
+    __syncthreads();                  // stage it visible; every wave is done with stage it-1
+    if (it + C::NS - 1 < ntiles) issue(it + C::NS - 1);  // into the slot of stage it-1
+  };
+  auto visible = [&](int it) { return !(a.causal && qstart + 64 * (ntiles - 1 - it) + 63 < kw); };
+#pragma unroll
+  for (int st = 0; st < C::NS - 1; ++st)
+    if (st < ntiles) issue(st);
+  int it = 0;
+  for (; it < it_a; ++it) {
+    step(it);
+    if (visible(it)) tile(it, std::true_type{});
   }
-  for (; j < n_full; ++j) {
-    if (j + 1 < ntiles) issue(j + 1);
-    tile(j, std::false_type{});
-    wait_dma();
-    __syncthreads();
+  for (; it < it_b; ++it) {
+    step(it);
+    tile(it, std::false_type{});
   }
-  for (; j < ntiles; ++j) {
-    if (j + 1 < ntiles) issue(j + 1);
-    tile(j, std::true_type{});
-    wait_dma();
-    __syncthreads();
+  for (; it < ntiles; ++it) {
+    step(it);
+    if (visible(it)) tile(it, std::true_type{});
   }
 
-  if constexpr (C::DT == 4) {
-    mfma_agpr_drain(adv[0], adv[1], adv[2], adv[3]);
-    mfma_agpr_drain(adk[0], adk[1], adk[2], adk[3]);
-  } else {
-    mfma_agpr_drain(adv[0], adv[1]);
-    mfma_agpr_drain(adk[0], adk[1]);
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    drain_all<C::DT>(adv[kb]);
+    drain_all<C::DT>(adk[kb]);
   }
-  if (kvrow < a.Sp) {
-    const int64_t col = (int64_t)b * a.Sp + kvrow;
-    bf16* dKt = (bf16*)a.dkt + (int64_t)h * DH * a.ld_dt + col;
-    bf16* dVt = (bf16*)a.dvt + (int64_t)h * DH * a.ld_dt + col;
 #pragma unroll
-    for (int t = 0; t < C::DT; ++t)
+  for (int kb = 0; kb < 2; ++kb) {
+    const int key = kw + 32 * kb + (lane & 31);
+    if (key < a.Sp) {
+      const int64_t col = (int64_t)b * a.Sp + key;
+      bf16* dKt = (bf16*)a.dkt + (int64_t)h * DH * a.ld_dt + col;
+      bf16* dVt = (bf16*)a.dvt + (int64_t)h * DH * a.ld_dt + col;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t d = 32 * t + acc_row(r, lane);
-        dKt[d * a.ld_dt] = (bf16)(adk[t][r] * scale);
-        dVt[d * a.ld_dt] = (bf16)adv[t][r];
-      }
+      for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t d = 32 * t + acc_row(r, lane);
+          dKt[d * a.ld_dt] = (bf16)(adk[kb][t][r] * scale);
+          dVt[d * a.ld_dt] = (bf16)adv[kb][t][r];
+        }
+    }
   }
 }
 
@@ -259,7 +285,8 @@ static hipError_t dkdv_launch(Dt dt, const AttnArgs& a, hipStream_t s) {
     auto k = attn_bwd_dkdv_bf16_kernel<DH>;
     hipError_t e = set_lds(k, DkvCfg<DH>::LDS);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k, dim3((unsigned)((a.Sp + 127) / 128), a.H, a.B), dim3(256), DkvCfg<DH>::LDS, s, a);
+    const int64_t nblk = (a.S + DkvCfg<DH>::KEYS - 1) / DkvCfg<DH>::KEYS;
+    hipLaunchKernelGGL(k, dim3((unsigned)(nblk * a.H * a.B)), dim3(256), DkvCfg<DH>::LDS, s, a);
   } else {
     const int lds = (2 * DH * 65 + 2 * 16 * DH + 32) * 4;
     hipError_t e = set_lds(attn_bwd_dkdv_f32_kernel<DH>, lds);

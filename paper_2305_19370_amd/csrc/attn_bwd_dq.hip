@@ -6,14 +6,19 @@
 namespace bpt {
 
 // ====================================================================== backward dQ, bf16
-// Query-outer: per query tile, loop over key tiles; S^T = K Q^T, dP^T = V dO^T,
-// dS^T = P^T (dP^T - Delta), dQ^T += K^T dS^T.
+// Query-outer: each wave owns 64 queries (two blocks of 32) and loops over key tiles
+// of 64: S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - Delta), dQ^T += K^T dS^T.
+// K^T fragments come from the K tile by transposing LDS reads; every fragment read
+// from LDS feeds the MFMAs of both query blocks.
 template <int DH>
 struct DqCfg {
   static constexpr int KSTEPS = DH / 16, DT = DH / 32;
-  static constexpr int RBYTES = RmTile<DH>::BYTES, FBYTES = FmTile<DH>::BYTES;
-  static constexpr int STAGE = 2 * RBYTES + FBYTES;   // K, V row-major; K^T feature-major
-  static constexpr int LDS = 2 * STAGE;
+  static constexpr int QROWS = 256;                 // queries per workgroup (4 waves x 64)
+  static constexpr int TB = RmTile<DH>::BYTES;
+  static constexpr int STAGE = 2 * TB;              // K and V tiles of 64 keys
+  static constexpr int NS = 4;                      // stages in the ring
+  static constexpr int LDS = NS * STAGE;
+  static constexpr int DPS = Ring2<DH>::DPW;        // copies per wave per stage
 };
 
 template <int DH>
@@ -22,12 +27,14 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int h = blockIdx.y, b = blockIdx.z;
   const int S = (int)a.S;
-  const int qt = a.causal ? (int)gridDim.x - 1 - (int)blockIdx.x : (int)blockIdx.x;
-  const int q0 = qt * 128;
-  const int qw = q0 + 32 * wave;
-  const int qrow = qw + (lane & 31);
+  const int nblk = (S + C::QROWS - 1) / C::QROWS;
+  int hh, blk;
+  xcd_map((int)blockIdx.x, nblk, a.H * a.B, hh, blk);
+  const int h = hh % a.H, b = hh / a.H;
+  const int qt = a.causal ? nblk - 1 - blk : blk;   // causal: the blocks with the most keys first
+  const int q0 = qt * C::QROWS;
+  const int qw = q0 + 64 * wave;
   const float scale = rsqrtf((float)DH);
   const float c = scale * LOG2E;
 
@@ -35,109 +42,126 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
   const bf16* Kb = (const bf16*)a.k + (int64_t)b * a.S * a.ld_k + h * DH;
   const bf16* Vb = (const bf16*)a.v + (int64_t)b * a.S * a.ld_v + h * DH;
   const bf16* dOb = (const bf16*)a.dout + (int64_t)b * a.S * a.ld_do + h * DH;
-  const bf16* Ktb = (const bf16*)a.kt + (int64_t)h * DH * a.ld_kt + (int64_t)b * a.Sp;
 
-  bf16x8 qf[C::KSTEPS], dof[C::KSTEPS];
-  {
-    const int qr = qrow < S ? qrow : S - 1;
+  bf16x8 qf[2][C::KSTEPS], dof[2][C::KSTEPS];
+  float nlse2[2], dl[2];
+  int kv_last[2];                                   // last key each lane's query may see (-1: none)
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int qrow = qw + 32 * qb + (lane & 31), qr = qrow < S ? qrow : S - 1;
+    const bool qok = qrow < S;
 #pragma unroll
     for (int kk = 0; kk < C::KSTEPS; ++kk) {
-      qf[kk] = __builtin_bit_cast(bf16x8, ld16(Qb + (int64_t)qr * a.ld_q + 16 * kk + 8 * (lane >> 5)));
-      dof[kk] = __builtin_bit_cast(bf16x8, ld16(dOb + (int64_t)qr * a.ld_do + 16 * kk + 8 * (lane >> 5)));
+      qf[qb][kk] = __builtin_bit_cast(bf16x8, ld16(Qb + (int64_t)qr * a.ld_q + 16 * kk + 8 * (lane >> 5)));
+      dof[qb][kk] = __builtin_bit_cast(bf16x8, ld16(dOb + (int64_t)qr * a.ld_do + 16 * kk + 8 * (lane >> 5)));
+      settle(qf[qb][kk]);
+      settle(dof[qb][kk]);
     }
+    const int64_t sidx = ((int64_t)b * a.H + h) * a.Sp + qr;
+    nlse2[qb] = qok ? -a.lse2[sidx] : 0.0f;
+    dl[qb] = qok ? a.delta[sidx] : 0.0f;
+    settle(nlse2[qb]);
+    settle(dl[qb]);
+    kv_last[qb] = !qok ? -1 : (a.causal ? qrow : S - 1);
   }
-  const int64_t sidx = ((int64_t)b * a.H + h) * a.Sp + qrow;
-  const bool qok = qrow < S;
-  const float nlse2 = qok ? -a.lse2[sidx] : 0.0f;
-  const float dl = qok ? a.delta[sidx] : 0.0f;
-  // last key this lane's query may see (-1: none)
-  const int kv_last = !qok ? -1 : (a.causal ? qrow : S - 1);
 
-  const int kv_end = a.causal ? (q0 + 128 < S ? q0 + 128 : S) : S;
+  const int kv_end = a.causal ? (q0 + C::QROWS < S ? q0 + C::QROWS : S) : S;
   const int ntiles = (kv_end + 63) / 64;
-  DmaPlan<RmTile<DH>::BLOCKS> pk, pv;
-  DmaPlan<FmTile<DH>::BLOCKS> pkt;
-  plan_rows<DH>(pk, (int)a.ld_k, wave, lane);
-  plan_rows<DH>(pv, (int)a.ld_v, wave, lane);
-  plan_cols<DH>(pkt, (int)a.ld_kt, wave, lane);
   auto issue = [&](int j) {
-    char* ks = smem + (j & 1) * C::STAGE;
-    dma_rows<DH>(ks, Kb, a.ld_k, j * 64, S - 1, wave, lane, pk);
-    dma_rows<DH>(ks + C::RBYTES, Vb, a.ld_v, j * 64, S - 1, wave, lane, pv);
-    dma_cols<DH>(ks + 2 * C::RBYTES, Ktb, j * 64, wave, pkt);
+    ring_issue<DH>(smem + (j % C::NS) * C::STAGE, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, S - 1, wave, lane);
   };
 
-  f32x16 acc[C::DT];
+  f32x16 acc[2][C::DT];                             // dQ^T of the two query blocks (AGPRs)
 #pragma unroll
-  for (int t = 0; t < C::DT; ++t) acc[t] = f32x16{};
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int t = 0; t < C::DT; ++t) mfma_agpr_zero(acc[qb][t]);
 
   auto tile = [&](int j, auto MASK) {
-    const int kv0 = j * 64;
-    const char* ks = smem + (j & 1) * C::STAGE;
-    const char* vs = ks + C::RBYTES;
-    const char* kts = vs + C::RBYTES;
-    const int lim = kv_last - kv0 - 4 * (lane >> 5);
+    const int kv0 = 64 * j;
+    const char* kt = smem + (j % C::NS) * C::STAGE;
+    const char* vt = kt + C::TB;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      f32x16 s = f32x16{}, dp = f32x16{};
+      f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
 #pragma unroll
       for (int kk = 0; kk < C::KSTEPS; ++kk) {
-        const int kc = 2 * kk + (lane >> 5);
-        const bf16x8 ak = *(const bf16x8*)(ks + rm_addr<DH>(32 * mt + (lane & 31), kc));
-        s = mfma32x32x16(ak, qf[kk], s);
-        const bf16x8 av = *(const bf16x8*)(vs + rm_addr<DH>(32 * mt + (lane & 31), kc));
-        dp = mfma32x32x16(av, dof[kk], dp);
+        const bf16x8 ak = frag_rows<DH>(kt, 32 * mt, 2 * kk, lane);
+        const bf16x8 av = frag_rows<DH>(vt, 32 * mt, 2 * kk, lane);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          s[qb] = mfma32x32x16(ak, qf[qb][kk], s[qb]);
+          dp[qb] = mfma32x32x16(av, dof[qb][kk], dp[qb]);
+        }
+        __builtin_amdgcn_sched_barrier(0);        // bound the fragments read ahead
       }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float p = fast_exp2(fmaf(s[r], c, nlse2));
-        if constexpr (decltype(MASK)::value) p = (32 * mt + 8 * (r >> 2) + (r & 3) <= lim) ? p : 0.0f;
-        s[r] = p * (dp[r] - dl);                    // dS^T
+      for (int qb = 0; qb < 2; ++qb) {
+        const int lim = kv_last[qb] - kv0 - 32 * mt;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float p = fast_exp2(fmaf(s[qb][r], c, nlse2[qb]));
+          if constexpr (decltype(MASK)::value) p = (acc_row(r, lane) <= lim) ? p : 0.0f;
+          s[qb][r] = p * (dp[qb][r] - dl[qb]);      // dS^T
+        }
       }
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        const bf16x8 sb = acc_to_b(s, hf);
+        const bf16x8 sb0 = acc_to_b(s[0], hf), sb1 = acc_to_b(s[1], hf);
 #pragma unroll
         for (int t = 0; t < C::DT; ++t) {
-          const bf16x8 af = fm_frag<DH>(kts, 32 * t + (lane & 31), 32 * mt + 16 * hf, lane);
-          acc[t] = mfma32x32x16(af, sb, acc[t]);
+          const bf16x8 kf = frag_tr<DH>(kt, 32 * mt + 16 * hf, 32 * t, lane);
+          mfma_agpr(acc[0][t], kf, sb0);
+          mfma_agpr(acc[1][t], kf, sb1);
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
     }
   };
 
-  // Key tiles every query of the workgroup fully sees come first (unmasked body);
-  // the diagonal and ragged tiles follow (masked body). Both loops are uniform over
-  // the workgroup, so every barrier is reached by all waves.
+  // Key tiles every query of the workgroup fully sees take the unmasked body; the
+  // diagonal and ragged tiles (and every tile of a block with queries past the end)
+  // take the masked one. Every barrier is reached by all waves.
   int n_full = a.causal ? std::min(ntiles, (q0 + 1) / 64) : ntiles;
   n_full = std::min(n_full, S / 64);
-  if (q0 + 128 > S) n_full = 0;
-  if (ntiles > 0) issue(0);
-  wait_dma();
-  __syncthreads();
+  if (q0 + C::QROWS > S) n_full = 0;
+#pragma unroll
+  for (int st = 0; st < C::NS - 1; ++st)
+    if (st < ntiles) issue(st);
+  auto step = [&](int j) {
+    // stage j has landed once at most the stages issued after it are pending
+    if (j + 2 < ntiles) wait_vmcnt<2 * C::DPS>();
+    else if (j + 1 < ntiles) wait_vmcnt<C::DPS>();
+    else wait_vmcnt<0>();
+    __syncthreads();                  // stage j visible; every wave is done with stage j-1
+    if (j + C::NS - 1 < ntiles) issue(j + C::NS - 1);   // into the slot of stage j-1
+  };
   int j = 0;
   for (; j < n_full; ++j) {
-    if (j + 1 < ntiles) issue(j + 1);
+    step(j);
     tile(j, std::false_type{});
-    wait_dma();
-    __syncthreads();
   }
   for (; j < ntiles; ++j) {
-    if (j + 1 < ntiles) issue(j + 1);
-    if (!(a.causal && j * 64 > qw + 31)) tile(j, std::true_type{});
-    wait_dma();
-    __syncthreads();
+    step(j);
+    if (!(a.causal && 64 * j > qw + 63)) tile(j, std::true_type{});
   }
 
-  if (qrow < a.Sp) {
-    bf16* dQt = (bf16*)a.dqt + (int64_t)h * DH * a.ld_dt + (int64_t)b * a.Sp + qrow;
 #pragma unroll
-    for (int t = 0; t < C::DT; ++t)
+  for (int qb = 0; qb < 2; ++qb) drain_all<C::DT>(acc[qb]);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int d = 32 * t + acc_row(r, lane);
-        dQt[(int64_t)d * a.ld_dt] = (bf16)(qok ? acc[t][r] * scale : 0.0f);
-      }
+  for (int qb = 0; qb < 2; ++qb) {
+    const int qrow = qw + 32 * qb + (lane & 31);
+    if (qrow < a.Sp) {
+      const bool qok = qrow < S;
+      bf16* dQt = (bf16*)a.dqt + (int64_t)h * DH * a.ld_dt + (int64_t)b * a.Sp + qrow;
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int d = 32 * t + acc_row(r, lane);
+          dQt[(int64_t)d * a.ld_dt] = (bf16)(qok ? acc[qb][t][r] * scale : 0.0f);
+        }
+    }
   }
 }
 
@@ -206,7 +230,8 @@ static hipError_t dq_launch(Dt dt, const AttnArgs& a, hipStream_t s) {
     auto k = attn_bwd_dq_bf16_kernel<DH>;
     hipError_t e = set_lds(k, DqCfg<DH>::LDS);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k, dim3((unsigned)((a.Sp + 127) / 128), a.H, a.B), dim3(256), DqCfg<DH>::LDS, s, a);
+    const int64_t nblk = (a.S + DqCfg<DH>::QROWS - 1) / DqCfg<DH>::QROWS;
+    hipLaunchKernelGGL(k, dim3((unsigned)(nblk * a.H * a.B)), dim3(256), DqCfg<DH>::LDS, s, a);
   } else {
     const int lds = (2 * DH * 65 + 2 * 16 * DH) * 4;
     hipError_t e = set_lds(attn_bwd_dq_f32_kernel<DH>, lds);

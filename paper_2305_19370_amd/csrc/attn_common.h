@@ -1,5 +1,6 @@
-// Device helpers shared by the attention kernels (LDS tile layouts, direct
-// global->LDS copies, MFMA fragment plumbing).
+// Device helpers shared by the attention kernels: the LDS tile layout, the ring of
+// direct global->LDS copies, MFMA fragment reads (plain and transposed), and the
+// workgroup -> (head, block) mapping.
 #pragma once
 
 #include <type_traits>
@@ -12,121 +13,113 @@ namespace bpt {
 static constexpr float LOG2E = 1.4426950408889634f;
 static constexpr float NEG_INF = -__builtin_inff();
 
-// LDS tile layouts. Rows are padded by one 16-byte slot so that the 32 rows a
-// fragment read touches start in different banks, and every fragment address is
-// one per-lane base plus a compile-time offset.
-//  * row-major tile: 64 rows of DH bf16 (DH/8 data slots + 1 pad slot per row);
-//  * feature-major tile: DH rows of 64 tokens (8 data slots + 1 pad slot per row).
+// Row-major LDS tile: 64 token rows of DH bf16 features. The pitch (DH*2 + 48 bytes
+// for DH = 128, DH*2 + 16 for DH = 64) is an odd multiple of 16 bytes, so the 16 rows
+// of a 16-byte fragment read start in distinct bank groups, and it spreads the four
+// 32-byte row pieces of a transposed read over distinct banks as well. Every fragment
+// address is a per-lane base plus a compile-time offset.
 template <int DH>
 struct RmTile {
-  static constexpr int SLOTS = DH / 8 + 1;
-  static constexpr int PITCH = SLOTS * 16;
+  static constexpr int PITCH = DH == 128 ? 304 : 144;
+  static constexpr int SLOTS = PITCH / 16;            // 16-byte slots per row
   static constexpr int BYTES = 64 * PITCH;
-  static constexpr int BLOCKS = BYTES / 1024;        // 1 KB blocks (one wave-wide copy each)
-  static_assert(BYTES % 1024 == 0, "tile must be whole 1 KB blocks");
+  static constexpr int BLOCKS = BYTES / 1024;         // 1 KiB blocks (one wave-wide copy each)
+  static_assert(DH == 64 || DH == 128, "head dim");
+  static_assert(BYTES % 1024 == 0, "tile must be whole 1 KiB blocks");
 };
-template <int DH>
-struct FmTile {
-  static constexpr int SLOTS = 9;
-  static constexpr int PITCH = SLOTS * 16;
-  static constexpr int BYTES = DH * PITCH;
-  static constexpr int BLOCKS = BYTES / 1024;
-  static_assert(BYTES % 1024 == 0, "tile must be whole 1 KB blocks");
-};
-
-// byte offset of 16-byte chunk kc of row `row` in a row-major tile
-template <int DH>
-BPT_DEV int rm_addr(int row, int kc) { return row * RmTile<DH>::PITCH + kc * 16; }
 
 BPT_DEV u32x4 ld16(const void* p) { return *(const u32x4*)p; }
 
-// Direct global -> LDS copy: every lane of the wave fetches 16 bytes from its own
-// address; lane l's bytes land at lds_block + 16 * l (lds_block is wave-uniform).
-// Inline assembly rather than the builtin: the compiler's counter tracking treats the
-// builtin as a pending FLAT access and then drains every later LDS-read wait to zero.
-// Completion is waited for by hand (wait_dma); M0 is otherwise unused in these kernels.
+// Force the completion of earlier global loads into v before the code that follows
+// (the compiler would otherwise place its own wait at the first use, inside a loop).
+BPT_DEV void settle(const bf16x8& v) { asm volatile("" ::"v"(v)); }
+BPT_DEV void settle(float v) { asm volatile("" ::"v"(v)); }
+
+// Direct global -> LDS copy: every lane of the wave fetches 16 (or 4) bytes from a
+// wave-uniform base address (SGPR pair) plus its own 32-bit byte offset; lane l's
+// bytes land at lds_block + 16 l (4 l). Inline assembly rather than the builtin: the
+// compiler's counter tracking treats the builtin as a pending FLAT access and then
+// drains every later LDS-read wait to zero. Completion is waited for by hand
+// (wait_vmcnt); M0 is not otherwise used in these kernels.
 BPT_DEV uint32_t lds_addr(const char* p) {
   return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)p);
 }
-BPT_DEV void dma16(const void* g, char* lds_block) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(g), "s"(lds_addr(lds_block)) : "memory");
+BPT_DEV void dma16s(const void* sbase, uint32_t voff, char* lds_block) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(voff), "s"(sbase), "s"(lds_addr(lds_block)) : "memory");
 }
-BPT_DEV void dma4(const void* g, char* lds_block) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
-               :: "v"(g), "s"(lds_addr(lds_block)) : "memory");
+BPT_DEV void dma4s(const void* sbase, uint32_t voff, char* lds_block) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :: "v"(voff), "s"(sbase), "s"(lds_addr(lds_block)) : "memory");
 }
-BPT_DEV void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+template <int N> BPT_DEV void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
 BPT_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }   // v_exp_f32; exp2(-inf) = 0
 
-// Copies of [64][DH] row-major tiles and [DH][64] feature-major tiles into LDS by the
-// 4 waves of a workgroup. Each wave copies the 1 KB blocks wave, wave + 4, ...; the
-// per-lane source offsets (in elements, relative to the tile origin) are computed
-// once, so a tile's copy only adds its origin. Pad slots re-fetch a data chunk of
-// the same row and are never read.
-template <int BLOCKS>
-struct DmaPlan {
-  static constexpr int MAXB = (BLOCKS + 3) / 4;
-  int off[MAXB];
+// Copies of stages made of two row-major tiles (rows row0 .. row0+63 of two tensors).
+// The 2 * BLOCKS copy blocks of a stage are dealt to the 4 waves round robin; every
+// wave issues the same number DPW (surplus slots repeat the last block, which writes
+// identical bytes), so a count of outstanding copies is the same on every wave. Pad
+// slots re-fetch a data chunk of the same row and are never read.
+template <int DH>
+struct Ring2 {
+  static constexpr int BL = RmTile<DH>::BLOCKS, NB = 2 * BL, DPW = (NB + 3) / 4;
 };
 
 template <int DH>
-BPT_DEV void plan_rows(DmaPlan<RmTile<DH>::BLOCKS>& p, int ld, int wave, int lane) {
+BPT_DEV int ring_block(int wave, int i) {
+  const int b = wave + 4 * i;
+  return b < Ring2<DH>::NB ? b : Ring2<DH>::NB - 1;
+}
+
+// Issue this wave's copies of one stage. Rows past last_row are clamped to it (the
+// kernels mask them); row0 <= last_row.
+template <int DH>
+BPT_DEV void ring_issue(char* stage, const bf16* src0, int ld0, const bf16* src1, int ld1,
+                        int row0, int last_row, int wave, int lane) {
   using T = RmTile<DH>;
+  const bf16* org0 = src0 + (int64_t)row0 * ld0;
+  const bf16* org1 = src1 + (int64_t)row0 * ld1;
+  const int lim = last_row - row0 < 63 ? last_row - row0 : 63;
+  // recomputed at every call: hoisting the offsets out of the tile loop would cost
+  // one register each for the whole kernel
+  asm volatile("" : "+v"(lane));
 #pragma unroll
-  for (int i = 0; i < p.MAXB; ++i) {
-    const int slot = (wave + 4 * i) * 64 + lane;
-    const int row = slot / T::SLOTS, col = slot % T::SLOTS;
-    p.off[i] = row * ld + (col < DH / 8 ? col : 0) * 8;
+  for (int i = 0; i < Ring2<DH>::DPW; ++i) {
+    const int b = ring_block<DH>(wave, i), t = b >= T::BLOCKS, blk = b - t * T::BLOCKS;
+    const int slot = blk * 64 + lane, col = slot % T::SLOTS;
+    int row = slot / T::SLOTS;
+    row = row < lim ? row : lim;
+    const uint32_t off = 2u * (uint32_t)(row * (t ? ld1 : ld0) + (col < DH / 8 ? col : 0) * 8);
+    dma16s(t ? org1 : org0, off, stage + t * T::BYTES + blk * 1024);
   }
 }
 
+// A-operand fragment with tile rows as MFMA rows: lane l reads row (row0 + l%32),
+// features 8*kc' .. 8*kc'+7 where kc' = kc + l/32 (kc even).
 template <int DH>
-BPT_DEV void plan_cols(DmaPlan<FmTile<DH>::BLOCKS>& p, int ld, int wave, int lane) {
-  using T = FmTile<DH>;
-#pragma unroll
-  for (int i = 0; i < p.MAXB; ++i) {
-    const int slot = (wave + 4 * i) * 64 + lane;
-    const int row = slot / T::SLOTS, col = slot % T::SLOTS;
-    p.off[i] = row * ld + (col < 8 ? col : 0) * 8;
-  }
+BPT_DEV bf16x8 frag_rows(const char* tile, int row0, int kc, int lane) {
+  return *(const bf16x8*)(tile + (row0 + (lane & 31)) * RmTile<DH>::PITCH + (kc + (lane >> 5)) * 16);
 }
 
-// Rows row0 .. row0+63 of a row-major tensor; rows past last_row are clamped to it
-// (callers mask them).
-template <int DH>
-BPT_DEV void dma_rows(char* tile, const bf16* base, int64_t ld, int row0, int last_row, int wave, int lane,
-                      const DmaPlan<RmTile<DH>::BLOCKS>& p) {
-  using T = RmTile<DH>;
-  if (row0 + 63 <= last_row) {
-    const bf16* org = base + (int64_t)row0 * ld;
-#pragma unroll
-    for (int i = 0; i < p.MAXB; ++i)
-      if (wave + 4 * i < T::BLOCKS) dma16(org + p.off[i], tile + (wave + 4 * i) * 1024);
-  } else {
-#pragma unroll
-    for (int i = 0; i < p.MAXB; ++i) {
-      const int blk = wave + 4 * i;
-      if (blk >= T::BLOCKS) continue;
-      const int slot = blk * 64 + lane;
-      const int row = slot / T::SLOTS, col = slot % T::SLOTS;
-      int r = row0 + row;
-      r = r < last_row ? r : last_row;
-      dma16(base + (int64_t)r * ld + (col < DH / 8 ? col : 0) * 8, tile + blk * 1024);
-    }
-  }
-}
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4;
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short s16x8;
 
-// Columns tok0 .. tok0+63 of a feature-major tensor (always in bounds: the padded
-// width is a multiple of 64 and the padding is zero).
+// A-operand fragment of the transposed tile for a contraction over 16 tile rows:
+// lane l supplies feature d0 + l%32 at rows tok0 + 4*(l/32) + {0..3} and
+// tok0 + 8 + 4*(l/32) + {0..3}, the order in which an MFMA accumulator hands its rows
+// to the next MFMA as a B operand. Two ds_read_b64_tr_b16: inside each group of 16
+// lanes, lane m addresses 4 features of one row (row m/4, features 4*(m%4)..), and
+// the instruction returns to lane m feature m of rows 0..3 of the group.
 template <int DH>
-BPT_DEV void dma_cols(char* tile, const bf16* base, int tok0, int wave, const DmaPlan<FmTile<DH>::BLOCKS>& p) {
-  using T = FmTile<DH>;
-  const bf16* org = base + tok0;
-#pragma unroll
-  for (int i = 0; i < p.MAXB; ++i)
-    if (wave + 4 * i < T::BLOCKS) dma16(org + p.off[i], tile + (wave + 4 * i) * 1024);
+BPT_DEV bf16x8 frag_tr(const char* tile, int tok0, int d0, int lane) {
+  const int g = lane >> 4, m = lane & 15;
+  const char* p = tile + (tok0 + 4 * (g >> 1) + (m >> 2)) * RmTile<DH>::PITCH + (d0 + 16 * (g & 1) + 4 * (m & 3)) * 2;
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 8 * RmTile<DH>::PITCH));
+  const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
 }
 
 // max(v[l], v[l ^ 32]) for every lane l, without LDS.
@@ -137,16 +130,6 @@ BPT_DEV float max_halves(float v) {
 BPT_DEV float sum_halves(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
-// A-operand fragment for a contraction over 16 tokens starting at `tok0` (a multiple
-// of 16) of a feature-major LDS tile: lane l supplies row (row0 + l%32) at tokens
-// tok0 + 4*(l/32) + {0..3} and tok0 + 8 + 4*(l/32) + {0..3}, matching the order in
-// which an MFMA accumulator hands its rows to the next MFMA as a B operand. The tile
-// holds its tokens in tok_perm order, which makes these 8 tokens one 16-byte chunk.
-template <int DH>
-BPT_DEV bf16x8 fm_frag(const char* tile, int row, int tok0, int lane) {
-  return *(const bf16x8*)(tile + row * FmTile<DH>::PITCH + (tok0 + 8 * (lane >> 5)) * 2);
 }
 
 // Registers 8*hf .. 8*hf+7 of an accumulator as a bf16 B operand.
@@ -178,10 +161,29 @@ BPT_DEV void mfma_agpr_drain(f32x16& a0, f32x16& a1, f32x16& a2, f32x16& a3) {
 BPT_DEV void mfma_agpr_drain(f32x16& a0, f32x16& a1) {
   asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 7" : "+a"(a0), "+a"(a1));
 }
+template <int DT>
+BPT_DEV void drain_all(f32x16 (&a)[DT]) {
+  if constexpr (DT == 4) mfma_agpr_drain(a[0], a[1], a[2], a[3]);
+  else mfma_agpr_drain(a[0], a[1]);
+}
 
 // Row of accumulator register r for lane `lane` inside a 32x32 tile.
 BPT_DEV int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
+// Workgroup id -> (head instance hh in [0, NH), block in [0, nblk)). Workgroup i runs
+// on XCD i % 8 and every XCD has its own L2; when NH is a multiple of 8, all blocks of
+// a head run on one XCD, so the blocks that stream the same K/V (or Q/dO) tiles share
+// that L2. Block 0 of every head is dispatched first.
+BPT_DEV void xcd_map(int id, int nblk, int NH, int& hh, int& blk) {
+  if ((NH & 7) == 0) {
+    const int x = id & 7, k = id >> 3, hp = NH >> 3;
+    hh = x + 8 * (k % hp);
+    blk = k / hp;
+  } else {
+    hh = id % NH;
+    blk = id / NH;
+  }
+}
 
 template <typename K>
 static hipError_t set_lds(K kern, int bytes) {

@@ -11,8 +11,11 @@
 //  * the accumulator of S^T is, after exp and bf16 rounding, directly the B
 //    operand of O^T[d, q] += V^T[d, kv] P^T[kv, q] (the K index order inside one
 //    MFMA is permuted consistently on the A side), so P never touches LDS;
-//  * K and V^T tiles of 64 keys are staged in double-buffered LDS with a 16-byte
-//    chunk XOR swizzle; scores use exp2 with log2(e)/sqrt(dh) folded in one FMA.
+//  * K and V tiles of 64 keys (token-major, as the projections write them) stream
+//    through a 4-stage LDS ring filled by direct global->LDS copies; V^T fragments
+//    come from the V tile by transposing LDS reads;
+//  * each wave owns 64 queries, so every K or V fragment read from LDS feeds two
+//    MFMAs; scores use exp2 with log2(e)/sqrt(dh) folded in one FMA.
 // fp32 kernels: one query (or key) row per thread with VALU FMAs; used by the
 // fp32 parity workload.
 #include <algorithm>
@@ -25,9 +28,12 @@ namespace bpt {
 template <int DH>
 struct FwdCfg {
   static constexpr int KSTEPS = DH / 16, DT = DH / 32;
-  static constexpr int KBYTES = RmTile<DH>::BYTES, VBYTES = FmTile<DH>::BYTES;
-  static constexpr int STAGE = KBYTES + VBYTES;
-  static constexpr int LDS = 2 * STAGE;
+  static constexpr int QROWS = 256;                 // queries per workgroup (4 waves x 64)
+  static constexpr int TB = RmTile<DH>::BYTES;
+  static constexpr int STAGE = 2 * TB;              // K and V tiles of 64 keys
+  static constexpr int NS = 4;                      // stages in the ring
+  static constexpr int LDS = NS * STAGE;
+  static constexpr int DPS = Ring2<DH>::DPW;        // copies per wave per stage
 };
 
 // Largest exponent growth (base 2) tolerated before the running numerator is
@@ -36,150 +42,178 @@ struct FwdCfg {
 static constexpr float RESCALE_LOG2 = 8.0f;
 
 template <int DH>
-__global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
   using C = FwdCfg<DH>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int h = blockIdx.y, b = a.b_begin + blockIdx.z;
   const int S = (int)a.S;
-  // causal: the query tiles with the most keys are dispatched first
-  const int qt = a.causal ? (int)gridDim.x - 1 - (int)blockIdx.x : (int)blockIdx.x;
-  const int q0 = (int)a.q_begin + qt * 128;
-  const int qw = q0 + 32 * wave;
-  const int qrow = qw + (lane & 31);
+  const int nblk = (int)((a.q_end - a.q_begin + C::QROWS - 1) / C::QROWS);
+  int hh, blk;
+  xcd_map((int)blockIdx.x, nblk, a.H * a.nb, hh, blk);
+  const int h = hh % a.H, b = a.b_begin + hh / a.H;
+  const int qt = a.causal ? nblk - 1 - blk : blk;   // causal: the blocks with the most keys first
+  const int q0 = (int)a.q_begin + qt * C::QROWS;
+  const int qw = q0 + 64 * wave;                    // first query of this wave
   const float scale = rsqrtf((float)DH);
   const float c = scale * LOG2E;
 
   const bf16* Qb = (const bf16*)a.q + (int64_t)b * a.S * a.ld_q + h * DH;
   const bf16* Kb = (const bf16*)a.k + (int64_t)b * a.S * a.ld_k + h * DH;
-  const bf16* Vtb = (const bf16*)a.vt + (int64_t)h * DH * a.ld_vt + (int64_t)b * a.Sp;
+  const bf16* Vb = (const bf16*)a.v + (int64_t)b * a.S * a.ld_v + h * DH;
 
-  bf16x8 qf[C::KSTEPS];
-  {
-    const int qr = qrow < S ? qrow : S - 1;
+  // the wave's 64 queries (two blocks of 32, one per lane column) as B operands
+  bf16x8 qf[2][C::KSTEPS];
+  int kv_last[2];                                   // last key each lane's query may see
 #pragma unroll
-    for (int kk = 0; kk < C::KSTEPS; ++kk)
-      qf[kk] = __builtin_bit_cast(bf16x8, ld16(Qb + (int64_t)qr * a.ld_q + 16 * kk + 8 * (lane >> 5)));
-  }
-  // last key this lane's query may see
-  const int kv_last = a.causal ? (qrow < S - 1 ? qrow : S - 1) : S - 1;
-
-  const int kv_end = a.causal ? (q0 + 128 < S ? q0 + 128 : S) : S;
-  const int ntiles = (kv_end + 63) / 64;
-  DmaPlan<RmTile<DH>::BLOCKS> pk;
-  DmaPlan<FmTile<DH>::BLOCKS> pv;
-  plan_rows<DH>(pk, (int)a.ld_k, wave, lane);
-  plan_cols<DH>(pv, (int)a.ld_vt, wave, lane);
-  auto issue = [&](int j) {
-    char* kt = smem + (j & 1) * C::STAGE;
-    dma_rows<DH>(kt, Kb, a.ld_k, j * 64, S - 1, wave, lane, pk);
-    dma_cols<DH>(kt + C::KBYTES, Vtb, j * 64, wave, pv);
-  };
-
-  f32x16 acc[C::DT];
-#pragma unroll
-  for (int t = 0; t < C::DT; ++t) acc[t] = f32x16{};
-  float m_run = NEG_INF, l_run = 0.0f;
-
-  auto tile = [&](int j, auto MASK) {
-    const int kv0 = j * 64;
-    const char* kt = smem + (j & 1) * C::STAGE;
-    const char* vt = kt + C::KBYTES;
-    f32x16 s[2] = {f32x16{}, f32x16{}};
+  for (int qb = 0; qb < 2; ++qb) {
+    const int qrow = qw + 32 * qb + (lane & 31), qr = qrow < S ? qrow : S - 1;
 #pragma unroll
     for (int kk = 0; kk < C::KSTEPS; ++kk) {
-      const int kc = 2 * kk + (lane >> 5);
+      qf[qb][kk] = __builtin_bit_cast(bf16x8, ld16(Qb + (int64_t)qr * a.ld_q + 16 * kk + 8 * (lane >> 5)));
+      settle(qf[qb][kk]);
+    }
+    kv_last[qb] = a.causal ? qr : S - 1;
+  }
+
+  const int kv_end = a.causal ? (q0 + C::QROWS < S ? q0 + C::QROWS : S) : S;
+  const int ntiles = (kv_end + 63) / 64;
+  auto issue = [&](int j) {
+    ring_issue<DH>(smem + (j % C::NS) * C::STAGE, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, S - 1, wave, lane);
+  };
+
+  f32x16 acc[2][C::DT];                             // O^T of the two query blocks (AGPRs)
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int t = 0; t < C::DT; ++t) mfma_agpr_zero(acc[qb][t]);
+  float m_run[2] = {NEG_INF, NEG_INF}, l_run[2] = {0.0f, 0.0f};
+
+  auto tile = [&](int j, auto MASK) {
+    const int kv0 = 64 * j;
+    const char* kt = smem + (j % C::NS) * C::STAGE;
+    const char* vt = kt + C::TB;
+    // S^T[key, query] = K Q^T: each K fragment feeds both query blocks
+    f32x16 s[2][2] = {{f32x16{}, f32x16{}}, {f32x16{}, f32x16{}}};   // [key half][query block]
+#pragma unroll
+    for (int kk = 0; kk < C::KSTEPS; ++kk)
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
-        const bf16x8 af = *(const bf16x8*)(kt + rm_addr<DH>(32 * mt + (lane & 31), kc));
-        s[mt] = mfma32x32x16(af, qf[kk], s[mt]);
+        const bf16x8 af = frag_rows<DH>(kt, 32 * mt, 2 * kk, lane);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) s[mt][qb] = mfma32x32x16(af, qf[qb][kk], s[mt][qb]);
+        __builtin_amdgcn_sched_barrier(0);        // bound the fragments read ahead
+      }
+    if constexpr (decltype(MASK)::value) {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        const int lim = kv_last[qb] - kv0;
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            s[mt][qb][r] = (32 * mt + acc_row(r, lane) <= lim) ? s[mt][qb][r] : NEG_INF;
       }
     }
-    if constexpr (decltype(MASK)::value) {
-      // key offset inside the tile of register r is 32*mt + 8*(r/4) + (r%4) + 4*(lane/32)
-      const int lim = kv_last - kv0 - 4 * (lane >> 5);
+    float mx[2];
+    bool up[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      float m = NEG_INF;
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          s[mt][r] = (32 * mt + 8 * (r >> 2) + (r & 3) <= lim) ? s[mt][r] : NEG_INF;
+        for (int r = 0; r < 16; ++r) m = fmaxf(m, s[mt][qb][r]);
+      mx[qb] = max_halves(m);
+      up[qb] = (mx[qb] - m_run[qb]) * c > RESCALE_LOG2;   // true on the first visible tile
     }
-    float mx = NEG_INF;
+    if (__ballot(up[0] || up[1])) {
+      asm volatile("" ::: "memory");                      // keep the rescale behind the branch
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
+      for (int qb = 0; qb < 2; ++qb) {
+        const float corr = up[qb] ? fast_exp2((m_run[qb] - mx[qb]) * c) : 1.0f;   // exp2(-inf) = 0
+        l_run[qb] *= corr;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
-    mx = max_halves(mx);
-    const bool up = (mx - m_run) * c > RESCALE_LOG2;      // true on the first visible tile
-    if (__ballot(up)) {
-      asm volatile("" ::: "memory");                       // keep the rescale behind the branch
-      const float corr = up ? fast_exp2((m_run - mx) * c) : 1.0f;   // exp2(-inf) = 0
-      l_run *= corr;
-#pragma unroll
-      for (int t = 0; t < C::DT; ++t) acc[t] *= corr;
-    }
-    if (up) m_run = mx;
-    const float mc = (m_run == NEG_INF ? 0.0f : m_run) * c;
-    float rs = 0.0f;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(fmaf(s[mt][r], c, -mc));
-        s[mt][r] = p;
-        rs += p;
+        for (int t = 0; t < C::DT; ++t) acc[qb][t] *= corr;
       }
-    l_run += rs;
+    }
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      if (up[qb]) m_run[qb] = mx[qb];
+      const float mc = (m_run[qb] == NEG_INF ? 0.0f : m_run[qb]) * c;
+      float rs = 0.0f;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = fast_exp2(fmaf(s[mt][qb][r], c, -mc));
+          s[mt][qb][r] = p;
+          rs += p;
+        }
+      l_run[qb] += rs;
+    }
+    // O^T[d, query] += V^T P^T: each transposed V fragment feeds both query blocks
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        const bf16x8 pb = acc_to_b(s[mt], hf);
+        const bf16x8 p0 = acc_to_b(s[mt][0], hf), p1 = acc_to_b(s[mt][1], hf);
 #pragma unroll
         for (int t = 0; t < C::DT; ++t) {
-          const bf16x8 af = fm_frag<DH>(vt, 32 * t + (lane & 31), 32 * mt + 16 * hf, lane);
-          acc[t] = mfma32x32x16(af, pb, acc[t]);
+          const bf16x8 vf = frag_tr<DH>(vt, 32 * mt + 16 * hf, 32 * t, lane);
+          mfma_agpr(acc[0][t], vf, p0);
+          mfma_agpr(acc[1][t], vf, p1);
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
   };
 
-  // Key tiles every query of the workgroup fully sees come first (unmasked body);
-  // the diagonal and ragged tiles follow (masked body). Both loops are uniform over
-  // the workgroup, so every barrier is reached by all waves.
+  // Key tiles every query of the workgroup fully sees take the unmasked body; the
+  // diagonal and ragged tiles take the masked one. Every barrier is reached by all
+  // waves; a wave skips the arithmetic of tiles entirely after its queries.
   int n_full = a.causal ? std::min(ntiles, (q0 + 1) / 64) : ntiles;
   n_full = std::min(n_full, S / 64);
-  if (ntiles > 0) issue(0);
-  wait_dma();
-  __syncthreads();
+#pragma unroll
+  for (int st = 0; st < C::NS - 1; ++st)
+    if (st < ntiles) issue(st);
+  auto step = [&](int j) {
+    // stage j has landed once at most the stages issued after it are pending
+    if (j + 2 < ntiles) wait_vmcnt<2 * C::DPS>();
+    else if (j + 1 < ntiles) wait_vmcnt<C::DPS>();
+    else wait_vmcnt<0>();
+    __syncthreads();                  // stage j visible; every wave is done with stage j-1
+    if (j + C::NS - 1 < ntiles) issue(j + C::NS - 1);   // into the slot of stage j-1
+  };
   int j = 0;
   for (; j < n_full; ++j) {
-    if (j + 1 < ntiles) issue(j + 1);
+    step(j);
     tile(j, std::false_type{});
-    wait_dma();
-    __syncthreads();
   }
   for (; j < ntiles; ++j) {
-    if (j + 1 < ntiles) issue(j + 1);
-    if (!(a.causal && j * 64 > qw + 31)) tile(j, std::true_type{});
-    wait_dma();
-    __syncthreads();
+    step(j);
+    if (!(a.causal && 64 * j > qw + 63)) tile(j, std::true_type{});
   }
 
-  const float l_tot = sum_halves(l_run);
-  if (qrow < (int)a.q_end && qrow < S) {
-    const float inv = 1.0f / l_tot;
-    bf16* Op = (bf16*)a.o + ((int64_t)b * a.S + qrow) * a.ld_o + h * DH;
 #pragma unroll
-    for (int t = 0; t < C::DT; ++t)
+  for (int qb = 0; qb < 2; ++qb) drain_all<C::DT>(acc[qb]);
 #pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        bf16x4 v;
+  for (int qb = 0; qb < 2; ++qb) {
+    const float l_tot = sum_halves(l_run[qb]);
+    const int qrow = qw + 32 * qb + (lane & 31);
+    if (qrow < (int)a.q_end && qrow < S) {
+      const float inv = 1.0f / l_tot;
+      bf16* Op = (bf16*)a.o + ((int64_t)b * a.S + qrow) * a.ld_o + h * DH;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = (bf16)(acc[t][4 * rg + e] * inv);
-        *(bf16x4*)(Op + 32 * t + 8 * rg + 4 * (lane >> 5)) = v;
-      }
-    if (lane < 32) a.lse[((int64_t)b * a.H + h) * a.Sp + qrow] = m_run * scale + logf(l_tot);
+      for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          bf16x4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = (bf16)(acc[qb][t][4 * rg + e] * inv);
+          *(bf16x4*)(Op + 32 * t + 8 * rg + 4 * (lane >> 5)) = v;
+        }
+      if (lane < 32) a.lse[((int64_t)b * a.H + h) * a.Sp + qrow] = m_run[qb] * scale + logf(l_tot);
+    }
   }
 }
 
@@ -193,7 +227,7 @@ __global__ __launch_bounds__(64) void attn_fwd_f32_kernel(AttnArgs a) {
   const float scale = rsqrtf((float)DH), c = scale * LOG2E;
   const float* Qp = (const float*)a.q + (int64_t)h * DH;
   const float* Kp = (const float*)a.k + (int64_t)h * DH;
-  const float* Vt = (const float*)a.vt + (int64_t)h * DH * a.ld_vt + (int64_t)b * a.Sp;
+  const float* Vp = (const float*)a.v + (int64_t)h * DH;
   float qr[DH], acc[DH];
 #pragma unroll
   for (int d = 0; d < DH; ++d) {
@@ -207,8 +241,7 @@ __global__ __launch_bounds__(64) void attn_fwd_f32_kernel(AttnArgs a) {
       const int r = i / DH, d = i % DH;
       const int64_t kv = kv0 + r;
       Ks[r][d] = kv < S ? Kp[(b * S + kv) * a.ld_k + d] : 0.0f;
-      const int d2 = i / 32, r2 = i % 32;
-      Vs[r2][d2] = (kv0 + r2 < S) ? Vt[(int64_t)d2 * a.ld_vt + kv0 + r2] : 0.0f;
+      Vs[r][d] = kv < S ? Vp[(b * S + kv) * a.ld_v + d] : 0.0f;
     }
     __syncthreads();
     float sc[32];
@@ -257,8 +290,8 @@ static hipError_t fwd_launch(Dt dt, const AttnArgs& a, hipStream_t s) {
     auto kern = attn_fwd_bf16_kernel<DH>;
     hipError_t e = set_lds(kern, FwdCfg<DH>::LDS);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3((unsigned)((nq + 127) / 128), a.H, a.nb), dim3(256),
-                       FwdCfg<DH>::LDS, s, a);
+    const int64_t nblk = (nq + FwdCfg<DH>::QROWS - 1) / FwdCfg<DH>::QROWS;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(nblk * a.H * a.nb)), dim3(256), FwdCfg<DH>::LDS, s, a);
   } else {
     hipLaunchKernelGGL(attn_fwd_f32_kernel<DH>, dim3((unsigned)((nq + 63) / 64), a.H, a.nb),
                        dim3(64), 0, s, a);

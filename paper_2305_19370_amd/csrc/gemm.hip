@@ -19,11 +19,10 @@ namespace bpt {
 template <int EPI, typename CT, typename RT>
 BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float v) {
   CT* C = (CT*)a.C + z * a.sC;
-  const int64_t sn = a.perm_cols ? tok_perm(n) : n;   // stored column
-  const int64_t idx = m * a.ldc + sn;
+  const int64_t idx = m * a.ldc + n;
   if (n >= a.N) {                                   // zero padding columns
     C[idx] = from_f32<CT>(0.0f);
-    if (EPI == EPI_GELU && a.C2) a.C2[z * a.sC2 + m * a.ldc2 + sn] = 0.0f;
+    if (EPI == EPI_GELU && a.C2) a.C2[z * a.sC2 + m * a.ldc2 + n] = 0.0f;
     return;
   }
   if constexpr (EPI == EPI_STORE) {
@@ -39,7 +38,7 @@ BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float
   } else if constexpr (EPI == EPI_GELU) {
     if (a.bias) v += a.bias[a.bias_on_m ? m : n];
     C[idx] = from_f32<CT>(gelu_f(v));
-    if (a.C2) a.C2[z * a.sC2 + m * a.ldc2 + sn] = gelu_grad_f(v);
+    if (a.C2) a.C2[z * a.sC2 + m * a.ldc2 + n] = gelu_grad_f(v);
   } else {  // EPI_MUL
     const float* R = (const float*)a.R + z * a.sR;
     C[idx] = from_f32<CT>(v * R[m * a.ldr + n]);
@@ -73,9 +72,7 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
       if (n + e < ncols) epi_store<EPI, CT, RT>(a, z, m, n + e, v[e]);
     return;
   }
-  // a group of 4 columns maps onto a group of 4 under the token permutation
-  const int64_t sn = a.perm_cols ? tok_perm(n) : n;
-  CT* C = (CT*)a.C + z * a.sC + m * a.ldc + sn;
+  CT* C = (CT*)a.C + z * a.sC + m * a.ldc + n;
   if constexpr (EPI == EPI_STORE) {
     if constexpr (sizeof(CT) == 4) {
       if (a.accumulate) v += V4<CT>::ld(C);
@@ -92,7 +89,7 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
       f32x4 d;
 #pragma unroll
       for (int e = 0; e < 4; ++e) d[e] = gelu_grad_f(v[e]);
-      *(f32x4*)(a.C2 + z * a.sC2 + m * a.ldc2 + sn) = d;
+      *(f32x4*)(a.C2 + z * a.sC2 + m * a.ldc2 + n) = d;
     }
 #pragma unroll
     for (int e = 0; e < 4; ++e) v[e] = gelu_f(v[e]);

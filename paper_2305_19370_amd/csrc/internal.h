@@ -32,14 +32,7 @@ struct GemmArgs {
   int batch = 1;
   int accumulate = 0;          // fp32 C only: C += acc
   int bias_on_m = 0;           // EPI_GELU: bias indexed by row instead of column
-  int perm_cols = 0;           // store column n of C (and C2) at tok_perm(n)
 };
-
-// Token order of the feature-major bf16 operands of the attention kernels: inside
-// every aligned group of 16 tokens, bits 2 and 3 of the index are swapped, so the
-// 8 tokens one lane feeds into a 32x32x16 MFMA (t..t+3 and t+8..t+11) are adjacent.
-// The permutation is its own inverse.
-__host__ __device__ inline int64_t tok_perm(int64_t t) { return (t & ~(int64_t)12) | ((t & 4) << 1) | ((t & 8) >> 1); }
 
 // ab: element type of A and B. ct: type of C; rt: type of R.
 hipError_t gemm(Dt ab, Epi epi, Dt ct, Dt rt, const GemmArgs& a, hipStream_t s);
@@ -49,14 +42,10 @@ struct AttnArgs {
   // token-major tensors: token (b, s) is row b*S + s
   const void* q = nullptr;  int64_t ld_q = 0;    // pointer already at head 0's first column
   const void* k = nullptr;  int64_t ld_k = 0;
-  const void* v = nullptr;  int64_t ld_v = 0;    // token-major V (backward)
+  const void* v = nullptr;  int64_t ld_v = 0;
   const void* dout = nullptr; int64_t ld_do = 0;
   void* o = nullptr;        int64_t ld_o = 0;
-  // feature-major tensors: element (b, s, f) at row f, column b*Sp + s
-  const void* vt = nullptr; int64_t ld_vt = 0;
-  const void* qt = nullptr; int64_t ld_qt = 0;
-  const void* kt = nullptr; int64_t ld_kt = 0;
-  const void* dot = nullptr; int64_t ld_dot = 0;
+  // feature-major outputs: element (b, s, f) at row f, column b*Sp + s
   void* dqt = nullptr; void* dkt = nullptr; void* dvt = nullptr; int64_t ld_dt = 0;
   float* lse = nullptr;        // [B, H, Sp] natural log
   const float* delta = nullptr;// [B, H, Sp]
@@ -93,12 +82,9 @@ hipError_t layer_norm_param_grad(Dt ti, const void* x, const float* mu, const fl
                                  int64_t rows, int64_t D, hipStream_t s);
 
 // out[c, r] = in[r, c] for r < rows, 0 for rows <= r < rows_store; batched over z.
-// perm: TP_OUT stores output column r at tok_perm(r) (the output is a feature-major
-// attention operand); TP_IN reads input column c from tok_perm(c).
-enum { TP_OUT = 1, TP_IN = 2 };
 hipError_t transpose(Dt t, const void* in, int64_t ld_in, int64_t s_in, void* out, int64_t ld_out,
                      int64_t s_out, int64_t rows, int64_t cols, int64_t rows_store, int batch,
-                     hipStream_t s, int perm = 0);
+                     hipStream_t s);
 
 // out[r, c] = in[r, c]
 hipError_t copy2d(Dt t, const void* in, int64_t ld_in, void* out, int64_t ld_out, int64_t rows,

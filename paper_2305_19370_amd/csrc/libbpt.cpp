@@ -99,15 +99,14 @@ struct Bump {
 };
 
 struct SavedPtrs {
-  void *qk, *vt, *o;
+  void *qkv, *o;
   float *lse, *h, *mu1, *rstd1, *mu2, *rstd2;
 };
 
 SavedPtrs saved_layout(const Dims& d, void* base, int64_t* total) {
   Bump bp(base);
   SavedPtrs s;
-  s.qk = bp.take(d.T * 2 * d.D * d.E);
-  s.vt = bp.take(d.D * d.Tp * d.E);
+  s.qkv = bp.take(d.T * 3 * d.D * d.E);
   s.o = bp.take(d.T * d.D * d.E);
   s.lse = (float*)bp.take(d.B * d.H * d.Sp * 4);
   s.h = (float*)bp.take(d.T * d.D * 4);
@@ -120,14 +119,13 @@ SavedPtrs saved_layout(const Dims& d, void* base, int64_t* total) {
 }
 
 struct FwdWs {
-  void *wqkT, *wvT, *woT, *w1T, *w2T, *u, *vg, *gg;
+  void *wqkvT, *woT, *w1T, *w2T, *u, *vg, *gg;
 };
 
 FwdWs fwd_ws(const Dims& d, void* base, int64_t* total) {
   Bump bp(base);
   FwdWs w;
-  w.wqkT = bp.take(2 * d.D * d.D * d.E);
-  w.wvT = bp.take(d.D * d.D * d.E);
+  w.wqkvT = bp.take(3 * d.D * d.D * d.E);
   w.woT = bp.take(d.D * d.D * d.E);
   w.w1T = bp.take(d.F * d.D * d.E);
   w.w2T = bp.take(d.D * d.F * d.E);
@@ -143,7 +141,7 @@ struct BwdWs {
   void *vg, *vgT, *gT, *dzT, *dz, *dyT;
   float* gpT;
   float *dv, *dh, *dU, *delta, *lse2, *partial, *scratch;
-  void *dhe, *dhT, *oT, *dO, *dOT, *V, *qT, *kT, *dqkvT, *dqkv, *u, *uT;
+  void *dhe, *dhT, *oT, *dO, *dqkvT, *dqkv, *u, *uT;
 };
 
 BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
@@ -164,12 +162,8 @@ BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
   w.dhT = bp.take(d.D * d.Tp * d.E);
   w.oT = bp.take(d.D * d.Tp * d.E);
   w.dO = bp.take(d.T * d.D * d.E);
-  w.dOT = bp.take(d.D * d.Tp * d.E);
   w.delta = (float*)bp.take(d.B * d.H * d.Sp * 4);
   w.lse2 = (float*)bp.take(d.B * d.H * d.Sp * 4);
-  w.V = bp.take(d.T * d.D * d.E);
-  w.qT = bp.take(d.D * d.Tp * d.E);
-  w.kT = bp.take(d.D * d.Tp * d.E);
   w.dqkvT = bp.take(3 * d.D * d.Tp * d.E);
   w.dqkv = bp.take(d.T * 3 * d.D * d.E);
   w.u = bp.take(d.T * d.D * d.E);
@@ -270,8 +264,7 @@ bpt_status bpt_saved_layout_of(const bpt_config* cfg, bpt_saved_layout* out) {
   if (!out) return fail(BPT_ERR_INVALID_ARG, "out is NULL");
   int64_t total;
   SavedPtrs s = saved_layout(dims_of(*cfg), nullptr, &total);   // zero base: pointers are offsets
-  out->qk = (size_t)(uintptr_t)s.qk;
-  out->vt = (size_t)(uintptr_t)s.vt;
+  out->qkv = (size_t)(uintptr_t)s.qkv;
   out->o = (size_t)(uintptr_t)s.o;
   out->lse = (size_t)(uintptr_t)s.lse;
   out->h = (size_t)(uintptr_t)s.h;
@@ -392,30 +385,21 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
 
   // weights into the K-contiguous layouts the NT GEMMs read
   const double wb = 2.0 * E_;
-  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wq, D, 0, w.wqkT, D, 0, D, D, D, 1, s));
-  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wk, D, 0, off(w.wqkT, D * D * E_), D, 0, D, D, D, 1, s));
-  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wv, D, 0, w.wvT, D, 0, D, D, D, 1, s));
+  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wq, D, 0, w.wqkvT, D, 0, D, D, D, 1, s));
+  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wk, D, 0, off(w.wqkvT, D * D * E_), D, 0, D, D, D, 1, s));
+  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wv, D, 0, off(w.wqkvT, 2 * D * D * E_), D, 0, D, D, D, 1, s));
   RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wo, D, 0, w.woT, D, 0, D, D, D, 1, s));
   RUN("transpose.weights", 0, wb * D * F, transpose(E, p->W1, F, 0, w.w1T, D, 0, D, F, D, 1, s));
   RUN("transpose.weights", 0, wb * D * F, transpose(E, p->W2, D, 0, w.w2T, F, 0, F, D, F, 1, s));
 
-  // U = LN1(X); [Q | K] = U [Wq | Wk]; V^T = Wv^T U^T  (Algorithm 1: project the input)
+  // U = LN1(X); [Q | K | V] = U [Wq | Wk | Wv]  (Algorithm 1: project the input)
   RUN("layernorm.fwd", 0, 2.0 * T * D * E_,
       layer_norm(E, E, X, D, p->ln1_g, p->ln1_b, w.u, D, sv.mu1, sv.rstd1, T, D, cfg->ln_eps, 0, s));
   {
     GemmArgs g;
-    g.A = w.u; g.lda = D; g.B = w.wqkT; g.ldb = D; g.C = sv.qk; g.ldc = 2 * D;
-    g.M = T; g.N = 2 * D; g.K = D;
-    RUN("gemm.qk", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
-  }
-  {
-    GemmArgs g;
-    g.A = w.wvT; g.lda = D; g.sA = 0;
-    g.B = w.u; g.ldb = D; g.sB = d.S * D;
-    g.C = sv.vt; g.ldc = d.Tp; g.sC = d.Sp;
-    g.M = D; g.N = d.S; g.Nstore = d.Sp; g.K = D; g.batch = (int)d.B;
-    g.perm_cols = E == BF16;                      // attention operand token order
-    RUN("gemm.vt", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
+    g.A = w.u; g.lda = D; g.B = w.wqkvT; g.ldb = D; g.C = sv.qkv; g.ldc = 3 * D;
+    g.M = T; g.N = 3 * D; g.K = D;
+    RUN("gemm.qkv", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
   }
 
   // Outer loop over groups of query blocks: attention for the group, then the
@@ -425,9 +409,9 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
       const int64_t r = std::min(d.R, d.S - s0);
       const int64_t t0 = b * d.S + s0;
       AttnArgs a;
-      a.q = sv.qk; a.ld_q = 2 * D;
-      a.k = off(sv.qk, D * E_); a.ld_k = 2 * D;
-      a.vt = sv.vt; a.ld_vt = d.Tp;
+      a.q = sv.qkv; a.ld_q = 3 * D;
+      a.k = off(sv.qkv, D * E_); a.ld_k = 3 * D;
+      a.v = off(sv.qkv, 2 * D * E_); a.ld_v = 3 * D;
       a.o = sv.o; a.ld_o = D;
       a.lse = sv.lse;
       a.S = d.S; a.Sp = d.Sp; a.B = (int)d.B; a.H = (int)d.H; a.dh = (int)d.dh; a.causal = cfg->causal;
@@ -567,21 +551,12 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
 
   // ---- attention backward, probabilities rebuilt from the saved log-sum-exp
   RUN("attn.delta", 0, 2.0 * T * D * E_, attn_delta(E, w.dO, sv.o, D, sv.lse, w.delta, w.lse2, B, S, Sp, (int)d.H, (int)d.dh, s));
-  // feature-major attention operands of the bf16 kernels use the permuted token order
-  const int tpo = E == BF16 ? TP_OUT : 0, tpi = E == BF16 ? TP_IN : 0;
-  RUN("transpose.act", 0, tb * T * D, transpose(E, sv.vt, Tp, Sp, w.V, D, S * D, D, S, D, B, s, tpi));
-  RUN("transpose.act", 0, tb * T * D, transpose(E, sv.qk, 2 * D, S * 2 * D, w.qT, Tp, Sp, S, D, Sp, B, s, tpo));
-  RUN("transpose.act", 0, tb * T * D, transpose(E, off(sv.qk, D * E_), 2 * D, S * 2 * D, w.kT, Tp, Sp, S, D, Sp, B, s, tpo));
-  RUN("transpose.act", 0, tb * T * D, transpose(E, w.dO, D, S * D, w.dOT, Tp, Sp, S, D, Sp, B, s, tpo));
   {
     AttnArgs a;
-    a.q = sv.qk; a.ld_q = 2 * D;
-    a.k = off(sv.qk, D * E_); a.ld_k = 2 * D;
-    a.v = w.V; a.ld_v = D;
+    a.q = sv.qkv; a.ld_q = 3 * D;
+    a.k = off(sv.qkv, D * E_); a.ld_k = 3 * D;
+    a.v = off(sv.qkv, 2 * D * E_); a.ld_v = 3 * D;
     a.dout = w.dO; a.ld_do = D;
-    a.qt = w.qT; a.ld_qt = Tp;
-    a.kt = w.kT; a.ld_kt = Tp;
-    a.dot = w.dOT; a.ld_dot = Tp;
     a.dqt = w.dqkvT; a.dkt = off(w.dqkvT, D * Tp * E_); a.dvt = off(w.dqkvT, 2 * D * Tp * E_); a.ld_dt = Tp;
     a.lse = sv.lse; a.delta = w.delta; a.lse2 = w.lse2;
     a.S = S; a.Sp = Sp; a.B = B; a.H = (int)d.H; a.dh = (int)d.dh; a.causal = cfg->causal;

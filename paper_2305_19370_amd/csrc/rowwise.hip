@@ -208,25 +208,22 @@ __global__ __launch_bounds__(256) void delta_kernel(const T* dO, const T* O, int
 template <typename T>
 __global__ __launch_bounds__(256) void transpose_kernel(const T* in, int64_t ld_in, int64_t s_in, T* out,
                                                         int64_t ld_out, int64_t s_out, int64_t rows,
-                                                        int64_t cols, int64_t rows_store, int perm) {
+                                                        int64_t cols, int64_t rows_store) {
   __shared__ T tile[64][65];
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
   in += (int64_t)blockIdx.z * s_in;
   out += (int64_t)blockIdx.z * s_out;
-  // column blocks are 64 wide, so the permutation stays inside the block
-  const int txi = (perm & TP_IN) ? (int)tok_perm(tx) : tx;
-  const int txo = (perm & TP_OUT) ? (int)tok_perm(tx) : tx;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const int64_t r = r0 + ty + 4 * i, c = c0 + tx;
-    tile[ty + 4 * i][tx] = (r < rows && c < cols) ? in[r * ld_in + c0 + txi] : from_f32<T>(0.0f);
+    tile[ty + 4 * i][tx] = (r < rows && c < cols) ? in[r * ld_in + c] : from_f32<T>(0.0f);
   }
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const int64_t c = c0 + ty + 4 * i, r = r0 + tx;
-    if (c < cols && r < rows_store) out[c * ld_out + r0 + txo] = tile[tx][ty + 4 * i];
+    if (c < cols && r < rows_store) out[c * ld_out + r] = tile[tx][ty + 4 * i];
   }
 }
 
@@ -317,11 +314,11 @@ hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, const f
 
 hipError_t transpose(Dt t, const void* in, int64_t ld_in, int64_t s_in, void* out, int64_t ld_out,
                      int64_t s_out, int64_t rows, int64_t cols, int64_t rows_store, int batch,
-                     hipStream_t s, int perm) {
+                     hipStream_t s) {
   if (cols <= 0 || rows_store <= 0 || batch <= 0) return hipSuccess;
   const dim3 grid((unsigned)((cols + 63) / 64), (unsigned)((rows_store + 63) / 64), (unsigned)batch);
   BPT_T(t, T, hipLaunchKernelGGL((transpose_kernel<T>), grid, dim3(256), 0, s, (const T*)in, ld_in, s_in,
-                                 (T*)out, ld_out, s_out, rows, cols, rows_store, perm));
+                                 (T*)out, ld_out, s_out, rows, cols, rows_store));
   return hipGetLastError();
 }
 

@@ -154,8 +154,7 @@ def test_saved_layout_offsets():
         assert lay["total"] == bpt.saved_bytes(c)
         es = 2 if dtype == "bf16" else 4
         T, D, Sp = 500, 256, 256
-        assert lay["vt"] - lay["qk"] >= T * 2 * D * es
-        assert lay["o"] - lay["vt"] >= D * 2 * Sp * es
+        assert lay["o"] - lay["qkv"] >= T * 3 * D * es
         assert lay["h"] - lay["lse"] >= 2 * 4 * Sp * 4
 
 
