@@ -17,10 +17,12 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 SOURCES = ["libbpt.cpp", "gemm.hip", "attn_fwd.hip", "attn_bwd_dq.hip", "attn_bwd_dkdv.hip", "rowwise.hip"]
-# per-source code generation options: the backward attention kernels keep their
-# MFMA accumulators in architectural VGPRs (the default placement copies them
-# between register files every iteration)
+# per-source code generation options: the attention kernels keep the accumulators of
+# their builtin MFMAs in architectural VGPRs (the default placement copies them
+# between register files every iteration; their long-lived accumulators are AGPRs
+# managed by inline assembly)
 EXTRA_FLAGS = {
+    "attn_fwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "attn_bwd_dq.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "attn_bwd_dkdv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }

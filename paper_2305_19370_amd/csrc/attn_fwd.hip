@@ -89,75 +89,67 @@ __global__ __launch_bounds__(256, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
     for (int t = 0; t < C::DT; ++t) mfma_agpr_zero(acc[qb][t]);
   float m_run[2] = {NEG_INF, NEG_INF}, l_run[2] = {0.0f, 0.0f};
 
+  // One key tile, as two halves of 32 keys; the running maximum is updated per half.
   auto tile = [&](int j, auto MASK) {
-    const int kv0 = 64 * j;
     const char* kt = smem + (j % C::NS) * C::STAGE;
     const char* vt = kt + C::TB;
-    // S^T[key, query] = K Q^T: each K fragment feeds both query blocks
-    f32x16 s[2][2] = {{f32x16{}, f32x16{}}, {f32x16{}, f32x16{}}};   // [key half][query block]
 #pragma unroll
-    for (int kk = 0; kk < C::KSTEPS; ++kk)
+    for (int mt = 0; mt < 2; ++mt) {
+      const int kv0 = 64 * j + 32 * mt;
+      // S^T[key, query] = K Q^T: each K fragment feeds both query blocks
+      f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
+      for (int kk = 0; kk < C::KSTEPS; ++kk) {
         const bf16x8 af = frag_rows<DH>(kt, 32 * mt, 2 * kk, lane);
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) s[mt][qb] = mfma32x32x16(af, qf[qb][kk], s[mt][qb]);
+        for (int qb = 0; qb < 2; ++qb) s[qb] = mfma32x32x16(af, qf[qb][kk], s[qb]);
         __builtin_amdgcn_sched_barrier(0);        // bound the fragments read ahead
       }
-    if constexpr (decltype(MASK)::value) {
+      if constexpr (decltype(MASK)::value) {
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          const int lim = kv_last[qb] - kv0;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s[qb][r] = (acc_row(r, lane) <= lim) ? s[qb][r] : NEG_INF;
+        }
+      }
+      float mx[2];
+      bool up[2];
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
-        const int lim = kv_last[qb] - kv0;
+        float m = NEG_INF;
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            s[mt][qb][r] = (32 * mt + acc_row(r, lane) <= lim) ? s[mt][qb][r] : NEG_INF;
+        for (int r = 0; r < 16; ++r) m = fmaxf(m, s[qb][r]);
+        mx[qb] = max_halves(m);
+        up[qb] = (mx[qb] - m_run[qb]) * c > RESCALE_LOG2;   // true on the first visible keys
       }
-    }
-    float mx[2];
-    bool up[2];
+      if (__ballot(up[0] || up[1])) {
+        asm volatile("" ::: "memory");                      // keep the rescale behind the branch
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      float m = NEG_INF;
+        for (int qb = 0; qb < 2; ++qb) {
+          const float corr = up[qb] ? fast_exp2((m_run[qb] - mx[qb]) * c) : 1.0f;   // exp2(-inf) = 0
+          l_run[qb] *= corr;
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) m = fmaxf(m, s[mt][qb][r]);
-      mx[qb] = max_halves(m);
-      up[qb] = (mx[qb] - m_run[qb]) * c > RESCALE_LOG2;   // true on the first visible tile
-    }
-    if (__ballot(up[0] || up[1])) {
-      asm volatile("" ::: "memory");                      // keep the rescale behind the branch
+          for (int t = 0; t < C::DT; ++t) acc[qb][t] *= corr;
+        }
+      }
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
-        const float corr = up[qb] ? fast_exp2((m_run[qb] - mx[qb]) * c) : 1.0f;   // exp2(-inf) = 0
-        l_run[qb] *= corr;
-#pragma unroll
-        for (int t = 0; t < C::DT; ++t) acc[qb][t] *= corr;
-      }
-    }
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      if (up[qb]) m_run[qb] = mx[qb];
-      const float mc = (m_run[qb] == NEG_INF ? 0.0f : m_run[qb]) * c;
-      float rs = 0.0f;
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
+        if (up[qb]) m_run[qb] = mx[qb];
+        const float mc = (m_run[qb] == NEG_INF ? 0.0f : m_run[qb]) * c;
+        float rs = 0.0f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(fmaf(s[mt][qb][r], c, -mc));
-          s[mt][qb][r] = p;
+          const float p = fast_exp2(fmaf(s[qb][r], c, -mc));
+          s[qb][r] = p;
           rs += p;
         }
-      l_run[qb] += rs;
-    }
-    // O^T[d, query] += V^T P^T: each transposed V fragment feeds both query blocks
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
+        l_run[qb] += rs;
+      }
+      // O^T[d, query] += V^T P^T: each transposed V fragment feeds both query blocks
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        const bf16x8 p0 = acc_to_b(s[mt][0], hf), p1 = acc_to_b(s[mt][1], hf);
+        const bf16x8 p0 = acc_to_b(s[0], hf), p1 = acc_to_b(s[1], hf);
 #pragma unroll
         for (int t = 0; t < C::DT; ++t) {
           const bf16x8 vf = frag_tr<DH>(vt, 32 * mt + 16 * hf, 32 * t, lane);
@@ -166,6 +158,7 @@ __global__ __launch_bounds__(256, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
           __builtin_amdgcn_sched_barrier(0);
         }
       }
+    }
   };
 
   // Key tiles every query of the workgroup fully sees take the unmasked body; the

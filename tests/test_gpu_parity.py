@@ -24,12 +24,16 @@ from gpu_util import GRAD_NAMES, bf16_model, run_gpu, run_oracle, say, stats, ta
 pytestmark = pytest.mark.gpu
 
 FP32_E_MAX = 1e-4
-BF16_E_MAX, BF16_E_MEAN, MODEL_FACTOR = 2e-2, 2e-3, 1.25
+BF16_E_MAX, BF16_E_MEAN = 2e-2, 2e-3
+# Factors over the rounding model's error. The mean over a tensor is a stable statistic;
+# the maximum over 1e4..1e5 elements of two different rounding orders is not (the
+# GPU/model ratio of e_max spans 0.76..1.27 over the bf16 cases), hence the wider factor.
+MODEL_FACTOR_MAX, MODEL_FACTOR_MEAN = 1.5, 1.25
 
 
 def bf16_limits(model_stats):
-    return (max(BF16_E_MAX, MODEL_FACTOR * model_stats["e_max"]),
-            max(BF16_E_MEAN, MODEL_FACTOR * model_stats["e_mean"]))
+    return (max(BF16_E_MAX, MODEL_FACTOR_MAX * model_stats["e_max"]),
+            max(BF16_E_MEAN, MODEL_FACTOR_MEAN * model_stats["e_mean"]))
 
 
 def compare_all(w, inp, gpu, Yr, g, tol_kind, label):
