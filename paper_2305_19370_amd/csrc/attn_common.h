@@ -57,24 +57,24 @@ template <int N> BPT_DEV void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" 
 BPT_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }   // v_exp_f32; exp2(-inf) = 0
 
 // Copies of stages made of two row-major tiles (rows row0 .. row0+63 of two tensors).
-// The 2 * BLOCKS copy blocks of a stage are dealt to the 4 waves round robin; every
+// The 2 * BLOCKS copy blocks of a stage are dealt to the NW waves round robin; every
 // wave issues the same number DPW (surplus slots repeat the last block, which writes
 // identical bytes), so a count of outstanding copies is the same on every wave. Pad
 // slots re-fetch a data chunk of the same row and are never read.
-template <int DH>
+template <int DH, int NW = 4>
 struct Ring2 {
-  static constexpr int BL = RmTile<DH>::BLOCKS, NB = 2 * BL, DPW = (NB + 3) / 4;
+  static constexpr int BL = RmTile<DH>::BLOCKS, NB = 2 * BL, DPW = (NB + NW - 1) / NW;
 };
 
-template <int DH>
+template <int DH, int NW>
 BPT_DEV int ring_block(int wave, int i) {
-  const int b = wave + 4 * i;
-  return b < Ring2<DH>::NB ? b : Ring2<DH>::NB - 1;
+  const int b = wave + NW * i;
+  return b < Ring2<DH, NW>::NB ? b : Ring2<DH, NW>::NB - 1;
 }
 
 // Issue this wave's copies of one stage. Rows past last_row are clamped to it (the
 // kernels mask them); row0 <= last_row.
-template <int DH>
+template <int DH, int NW = 4>
 BPT_DEV void ring_issue(char* stage, const bf16* src0, int ld0, const bf16* src1, int ld1,
                         int row0, int last_row, int wave, int lane) {
   using T = RmTile<DH>;
@@ -85,8 +85,8 @@ BPT_DEV void ring_issue(char* stage, const bf16* src0, int ld0, const bf16* src1
   // one register each for the whole kernel
   asm volatile("" : "+v"(lane));
 #pragma unroll
-  for (int i = 0; i < Ring2<DH>::DPW; ++i) {
-    const int b = ring_block<DH>(wave, i), t = b >= T::BLOCKS, blk = b - t * T::BLOCKS;
+  for (int i = 0; i < Ring2<DH, NW>::DPW; ++i) {
+    const int b = ring_block<DH, NW>(wave, i), t = b >= T::BLOCKS, blk = b - t * T::BLOCKS;
     const int slot = blk * 64 + lane, col = slot % T::SLOTS;
     int row = slot / T::SLOTS;
     row = row < lim ? row : lim;

@@ -14,8 +14,9 @@
 //  * K and V tiles of 64 keys (token-major, as the projections write them) stream
 //    through a 4-stage LDS ring filled by direct global->LDS copies; V^T fragments
 //    come from the V tile by transposing LDS reads;
-//  * each wave owns 64 queries, so every K or V fragment read from LDS feeds two
-//    MFMAs; scores use exp2 with log2(e)/sqrt(dh) folded in one FMA.
+//  * 8 waves of 32 queries share each stage; two waves per SIMD let one wave's
+//    softmax run while the other's MFMAs do; scores use exp2 with log2(e)/sqrt(dh)
+//    folded in one FMA.
 // fp32 kernels: one query (or key) row per thread with VALU FMAs; used by the
 // fp32 parity workload.
 #include <algorithm>
@@ -25,15 +26,18 @@
 namespace bpt {
 
 // ====================================================================== forward, bf16
+// 8 waves (two per SIMD, so that one wave's softmax overlaps the other's MFMAs), 32
+// queries per wave, 256 per workgroup; all waves share the K/V stages of the ring.
 template <int DH>
 struct FwdCfg {
   static constexpr int KSTEPS = DH / 16, DT = DH / 32;
-  static constexpr int QROWS = 256;                 // queries per workgroup (4 waves x 64)
+  static constexpr int NW = 8;                      // waves per workgroup
+  static constexpr int QROWS = 32 * NW;             // queries per workgroup
   static constexpr int TB = RmTile<DH>::BYTES;
   static constexpr int STAGE = 2 * TB;              // K and V tiles of 64 keys
   static constexpr int NS = 4;                      // stages in the ring
   static constexpr int LDS = NS * STAGE;
-  static constexpr int DPS = Ring2<DH>::DPW;        // copies per wave per stage
+  static constexpr int DPS = Ring2<DH, NW>::DPW;    // copies per wave per stage
 };
 
 // Largest exponent growth (base 2) tolerated before the running numerator is
@@ -42,7 +46,7 @@ struct FwdCfg {
 static constexpr float RESCALE_LOG2 = 8.0f;
 
 template <int DH>
-__global__ __launch_bounds__(256, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
+__global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
   using C = FwdCfg<DH>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -54,7 +58,8 @@ __global__ __launch_bounds__(256, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
   const int h = hh % a.H, b = a.b_begin + hh / a.H;
   const int qt = a.causal ? nblk - 1 - blk : blk;   // causal: the blocks with the most keys first
   const int q0 = (int)a.q_begin + qt * C::QROWS;
-  const int qw = q0 + 64 * wave;                    // first query of this wave
+  const int qw = q0 + 32 * wave;                    // first query of this wave
+  const int qrow = qw + (lane & 31);
   const float scale = rsqrtf((float)DH);
   const float c = scale * LOG2E;
 
@@ -62,103 +67,81 @@ __global__ __launch_bounds__(256, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
   const bf16* Kb = (const bf16*)a.k + (int64_t)b * a.S * a.ld_k + h * DH;
   const bf16* Vb = (const bf16*)a.v + (int64_t)b * a.S * a.ld_v + h * DH;
 
-  // the wave's 64 queries (two blocks of 32, one per lane column) as B operands
-  bf16x8 qf[2][C::KSTEPS];
-  int kv_last[2];                                   // last key each lane's query may see
+  // the wave's 32 queries (one per lane column) as B operands
+  bf16x8 qf[C::KSTEPS];
+  const int qr = qrow < S ? qrow : S - 1;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const int qrow = qw + 32 * qb + (lane & 31), qr = qrow < S ? qrow : S - 1;
-#pragma unroll
-    for (int kk = 0; kk < C::KSTEPS; ++kk) {
-      qf[qb][kk] = __builtin_bit_cast(bf16x8, ld16(Qb + (int64_t)qr * a.ld_q + 16 * kk + 8 * (lane >> 5)));
-      settle(qf[qb][kk]);
-    }
-    kv_last[qb] = a.causal ? qr : S - 1;
+  for (int kk = 0; kk < C::KSTEPS; ++kk) {
+    qf[kk] = __builtin_bit_cast(bf16x8, ld16(Qb + (int64_t)qr * a.ld_q + 16 * kk + 8 * (lane >> 5)));
+    settle(qf[kk]);
   }
+  const int kv_last = a.causal ? qr : S - 1;       // last key this lane's query may see
 
   const int kv_end = a.causal ? (q0 + C::QROWS < S ? q0 + C::QROWS : S) : S;
   const int ntiles = (kv_end + 63) / 64;
   auto issue = [&](int j) {
-    ring_issue<DH>(smem + (j % C::NS) * C::STAGE, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, S - 1, wave, lane);
+    ring_issue<DH, C::NW>(smem + (j % C::NS) * C::STAGE, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, S - 1, wave,
+                          lane);
   };
 
-  f32x16 acc[2][C::DT];                             // O^T of the two query blocks (AGPRs)
+  f32x16 acc[C::DT];                                // O^T of the wave's queries
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-    for (int t = 0; t < C::DT; ++t) mfma_agpr_zero(acc[qb][t]);
-  float m_run[2] = {NEG_INF, NEG_INF}, l_run[2] = {0.0f, 0.0f};
+  for (int t = 0; t < C::DT; ++t) acc[t] = f32x16{};
+  float m_run = NEG_INF, l_run = 0.0f;
 
-  // One key tile, as two halves of 32 keys; the running maximum is updated per half.
   auto tile = [&](int j, auto MASK) {
+    const int kv0 = 64 * j;
     const char* kt = smem + (j % C::NS) * C::STAGE;
     const char* vt = kt + C::TB;
+    // S^T[key, query] = K Q^T
+    f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-      const int kv0 = 64 * j + 32 * mt;
-      // S^T[key, query] = K Q^T: each K fragment feeds both query blocks
-      f32x16 s[2] = {f32x16{}, f32x16{}};
+    for (int kk = 0; kk < C::KSTEPS; ++kk)
 #pragma unroll
-      for (int kk = 0; kk < C::KSTEPS; ++kk) {
-        const bf16x8 af = frag_rows<DH>(kt, 32 * mt, 2 * kk, lane);
+      for (int mt = 0; mt < 2; ++mt) s[mt] = mfma32x32x16(frag_rows<DH>(kt, 32 * mt, 2 * kk, lane), qf[kk], s[mt]);
+    if constexpr (decltype(MASK)::value) {
+      const int lim = kv_last - kv0;
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) s[qb] = mfma32x32x16(af, qf[qb][kk], s[qb]);
-        __builtin_amdgcn_sched_barrier(0);        // bound the fragments read ahead
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[mt][r] = (32 * mt + acc_row(r, lane) <= lim) ? s[mt][r] : NEG_INF;
+    }
+    float mx = NEG_INF;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
+    mx = max_halves(mx);
+    const bool up = (mx - m_run) * c > RESCALE_LOG2;      // true on the first visible tile
+    if (__ballot(up)) {
+      asm volatile("" ::: "memory");                       // keep the rescale behind the branch
+      const float corr = up ? fast_exp2((m_run - mx) * c) : 1.0f;   // exp2(-inf) = 0
+      l_run *= corr;
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t) acc[t] *= corr;
+    }
+    if (up) m_run = mx;
+    const float mc = (m_run == NEG_INF ? 0.0f : m_run) * c;
+    float rs = 0.0f;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(fmaf(s[mt][r], c, -mc));
+        s[mt][r] = p;
+        rs += p;
       }
-      if constexpr (decltype(MASK)::value) {
+    l_run += rs;
+    // O^T[d, query] += V^T P^T, V^T fragments by transposing reads of the V tile
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          const int lim = kv_last[qb] - kv0;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) s[qb][r] = (acc_row(r, lane) <= lim) ? s[qb][r] : NEG_INF;
-        }
-      }
-      float mx[2];
-      bool up[2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        float m = NEG_INF;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) m = fmaxf(m, s[qb][r]);
-        mx[qb] = max_halves(m);
-        up[qb] = (mx[qb] - m_run[qb]) * c > RESCALE_LOG2;   // true on the first visible keys
-      }
-      if (__ballot(up[0] || up[1])) {
-        asm volatile("" ::: "memory");                      // keep the rescale behind the branch
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          const float corr = up[qb] ? fast_exp2((m_run[qb] - mx[qb]) * c) : 1.0f;   // exp2(-inf) = 0
-          l_run[qb] *= corr;
-#pragma unroll
-          for (int t = 0; t < C::DT; ++t) acc[qb][t] *= corr;
-        }
-      }
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        if (up[qb]) m_run[qb] = mx[qb];
-        const float mc = (m_run[qb] == NEG_INF ? 0.0f : m_run[qb]) * c;
-        float rs = 0.0f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(fmaf(s[qb][r], c, -mc));
-          s[qb][r] = p;
-          rs += p;
-        }
-        l_run[qb] += rs;
-      }
-      // O^T[d, query] += V^T P^T: each transposed V fragment feeds both query blocks
+    for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        const bf16x8 p0 = acc_to_b(s[0], hf), p1 = acc_to_b(s[1], hf);
+        const bf16x8 pb = acc_to_b(s[mt], hf);
 #pragma unroll
-        for (int t = 0; t < C::DT; ++t) {
-          const bf16x8 vf = frag_tr<DH>(vt, 32 * mt + 16 * hf, 32 * t, lane);
-          mfma_agpr(acc[0][t], vf, p0);
-          mfma_agpr(acc[1][t], vf, p1);
-          __builtin_amdgcn_sched_barrier(0);
-        }
+        for (int t = 0; t < C::DT; ++t)
+          acc[t] = mfma32x32x16(frag_tr<DH>(vt, 32 * mt + 16 * hf, 32 * t, lane), pb, acc[t]);
       }
-    }
   };
 
   // Key tiles every query of the workgroup fully sees take the unmasked body; the
@@ -184,29 +167,23 @@ __global__ __launch_bounds__(256, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
   }
   for (; j < ntiles; ++j) {
     step(j);
-    if (!(a.causal && 64 * j > qw + 63)) tile(j, std::true_type{});
+    if (!(a.causal && 64 * j > qw + 31)) tile(j, std::true_type{});
   }
 
+  const float l_tot = sum_halves(l_run);
+  if (qrow < (int)a.q_end && qrow < S) {
+    const float inv = 1.0f / l_tot;
+    bf16* Op = (bf16*)a.o + ((int64_t)b * a.S + qrow) * a.ld_o + h * DH;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) drain_all<C::DT>(acc[qb]);
+    for (int t = 0; t < C::DT; ++t)
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const float l_tot = sum_halves(l_run[qb]);
-    const int qrow = qw + 32 * qb + (lane & 31);
-    if (qrow < (int)a.q_end && qrow < S) {
-      const float inv = 1.0f / l_tot;
-      bf16* Op = (bf16*)a.o + ((int64_t)b * a.S + qrow) * a.ld_o + h * DH;
+      for (int rg = 0; rg < 4; ++rg) {
+        bf16x4 v;
 #pragma unroll
-      for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-          bf16x4 v;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = (bf16)(acc[qb][t][4 * rg + e] * inv);
-          *(bf16x4*)(Op + 32 * t + 8 * rg + 4 * (lane >> 5)) = v;
-        }
-      if (lane < 32) a.lse[((int64_t)b * a.H + h) * a.Sp + qrow] = m_run[qb] * scale + logf(l_tot);
-    }
+        for (int e = 0; e < 4; ++e) v[e] = (bf16)(acc[t][4 * rg + e] * inv);
+        *(bf16x4*)(Op + 32 * t + 8 * rg + 4 * (lane >> 5)) = v;
+      }
+    if (lane < 32) a.lse[((int64_t)b * a.H + h) * a.Sp + qrow] = m_run * scale + logf(l_tot);
   }
 }
 
@@ -284,7 +261,7 @@ static hipError_t fwd_launch(Dt dt, const AttnArgs& a, hipStream_t s) {
     hipError_t e = set_lds(kern, FwdCfg<DH>::LDS);
     if (e != hipSuccess) return e;
     const int64_t nblk = (nq + FwdCfg<DH>::QROWS - 1) / FwdCfg<DH>::QROWS;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(nblk * a.H * a.nb)), dim3(256), FwdCfg<DH>::LDS, s, a);
+    hipLaunchKernelGGL(kern, dim3((unsigned)(nblk * a.H * a.nb)), dim3(64 * FwdCfg<DH>::NW), FwdCfg<DH>::LDS, s, a);
   } else {
     hipLaunchKernelGGL(attn_fwd_f32_kernel<DH>, dim3((unsigned)((nq + 63) / 64), a.H, a.nb),
                        dim3(64), 0, s, a);
