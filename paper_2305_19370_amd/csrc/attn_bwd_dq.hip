@@ -6,23 +6,24 @@
 namespace bpt {
 
 // ====================================================================== backward dQ, bf16
-// Query-outer: each wave owns 64 queries (two blocks of 32) and loops over key tiles
-// of 64: S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - Delta), dQ^T += K^T dS^T.
-// K^T fragments come from the K tile by transposing LDS reads; every fragment read
-// from LDS feeds the MFMAs of both query blocks.
+// Query-outer: 8 waves (two per SIMD, so one wave's VALU work overlaps the other's
+// MFMAs) of 32 queries each, 256 per workgroup, loop over key tiles of 64:
+// S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - Delta), dQ^T += K^T dS^T. K^T
+// fragments come from the K tile by transposing LDS reads.
 template <int DH>
 struct DqCfg {
   static constexpr int KSTEPS = DH / 16, DT = DH / 32;
-  static constexpr int QROWS = 256;                 // queries per workgroup (4 waves x 64)
+  static constexpr int NW = 8;                      // waves per workgroup
+  static constexpr int QROWS = 32 * NW;             // queries per workgroup
   static constexpr int TB = RmTile<DH>::BYTES;
   static constexpr int STAGE = 2 * TB;              // K and V tiles of 64 keys
   static constexpr int NS = 4;                      // stages in the ring
   static constexpr int LDS = NS * STAGE;
-  static constexpr int DPS = Ring2<DH>::DPW;        // copies per wave per stage
+  static constexpr int DPS = Ring2<DH, NW>::DPW;    // copies per wave per stage
 };
 
 template <int DH>
-__global__ __launch_bounds__(256, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
+__global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
   using C = DqCfg<DH>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -34,7 +35,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
   const int h = hh % a.H, b = hh / a.H;
   const int qt = a.causal ? nblk - 1 - blk : blk;   // causal: the blocks with the most keys first
   const int q0 = qt * C::QROWS;
-  const int qw = q0 + 64 * wave;
+  const int qw = q0 + 32 * wave;
+  const int qrow = qw + (lane & 31);
   const float scale = rsqrtf((float)DH);
   const float c = scale * LOG2E;
 
@@ -43,39 +45,33 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
   const bf16* Vb = (const bf16*)a.v + (int64_t)b * a.S * a.ld_v + h * DH;
   const bf16* dOb = (const bf16*)a.dout + (int64_t)b * a.S * a.ld_do + h * DH;
 
-  bf16x8 qf[2][C::KSTEPS], dof[2][C::KSTEPS];
-  float nlse2[2], dl[2];
-  int kv_last[2];                                   // last key each lane's query may see (-1: none)
+  bf16x8 qf[C::KSTEPS], dof[C::KSTEPS];
+  const bool qok = qrow < S;
+  const int qr = qok ? qrow : S - 1;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const int qrow = qw + 32 * qb + (lane & 31), qr = qrow < S ? qrow : S - 1;
-    const bool qok = qrow < S;
-#pragma unroll
-    for (int kk = 0; kk < C::KSTEPS; ++kk) {
-      qf[qb][kk] = __builtin_bit_cast(bf16x8, ld16(Qb + (int64_t)qr * a.ld_q + 16 * kk + 8 * (lane >> 5)));
-      dof[qb][kk] = __builtin_bit_cast(bf16x8, ld16(dOb + (int64_t)qr * a.ld_do + 16 * kk + 8 * (lane >> 5)));
-      settle(qf[qb][kk]);
-      settle(dof[qb][kk]);
-    }
-    const int64_t sidx = ((int64_t)b * a.H + h) * a.Sp + qr;
-    nlse2[qb] = qok ? -a.lse2[sidx] : 0.0f;
-    dl[qb] = qok ? a.delta[sidx] : 0.0f;
-    settle(nlse2[qb]);
-    settle(dl[qb]);
-    kv_last[qb] = !qok ? -1 : (a.causal ? qrow : S - 1);
+  for (int kk = 0; kk < C::KSTEPS; ++kk) {
+    qf[kk] = __builtin_bit_cast(bf16x8, ld16(Qb + (int64_t)qr * a.ld_q + 16 * kk + 8 * (lane >> 5)));
+    dof[kk] = __builtin_bit_cast(bf16x8, ld16(dOb + (int64_t)qr * a.ld_do + 16 * kk + 8 * (lane >> 5)));
+    settle(qf[kk]);
+    settle(dof[kk]);
   }
+  const int64_t sidx = ((int64_t)b * a.H + h) * a.Sp + qr;
+  const float nlse2 = qok ? -a.lse2[sidx] : 0.0f;
+  const float dl = qok ? a.delta[sidx] : 0.0f;
+  settle(nlse2);
+  settle(dl);
+  const int kv_last = !qok ? -1 : (a.causal ? qrow : S - 1);   // last key this query may see
 
   const int kv_end = a.causal ? (q0 + C::QROWS < S ? q0 + C::QROWS : S) : S;
   const int ntiles = (kv_end + 63) / 64;
   auto issue = [&](int j) {
-    ring_issue<DH>(smem + (j % C::NS) * C::STAGE, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, S - 1, wave, lane);
+    ring_issue<DH, C::NW>(smem + (j % C::NS) * C::STAGE, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, S - 1, wave,
+                          lane);
   };
 
-  f32x16 acc[2][C::DT];                             // dQ^T of the two query blocks (AGPRs)
+  f32x16 acc[C::DT];                                // dQ^T of the wave's queries
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-    for (int t = 0; t < C::DT; ++t) mfma_agpr_zero(acc[qb][t]);
+  for (int t = 0; t < C::DT; ++t) acc[t] = f32x16{};
 
   auto tile = [&](int j, auto MASK) {
     const int kv0 = 64 * j;
@@ -83,45 +79,33 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
     const char* vt = kt + C::TB;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
+      f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < C::KSTEPS; ++kk) {
-        const bf16x8 ak = frag_rows<DH>(kt, 32 * mt, 2 * kk, lane);
-        const bf16x8 av = frag_rows<DH>(vt, 32 * mt, 2 * kk, lane);
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          s[qb] = mfma32x32x16(ak, qf[qb][kk], s[qb]);
-          dp[qb] = mfma32x32x16(av, dof[qb][kk], dp[qb]);
-        }
-        __builtin_amdgcn_sched_barrier(0);        // bound the fragments read ahead
+        s = mfma32x32x16(frag_rows<DH>(kt, 32 * mt, 2 * kk, lane), qf[kk], s);
+        dp = mfma32x32x16(frag_rows<DH>(vt, 32 * mt, 2 * kk, lane), dof[kk], dp);
       }
+      const int lim = kv_last - kv0 - 32 * mt;
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        const int lim = kv_last[qb] - kv0 - 32 * mt;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float p = fast_exp2(fmaf(s[qb][r], c, nlse2[qb]));
-          if constexpr (decltype(MASK)::value) p = (acc_row(r, lane) <= lim) ? p : 0.0f;
-          s[qb][r] = p * (dp[qb][r] - dl[qb]);      // dS^T
-        }
+      for (int r = 0; r < 16; ++r) {
+        float p = fast_exp2(fmaf(s[r], c, nlse2));
+        if constexpr (decltype(MASK)::value) p = (acc_row(r, lane) <= lim) ? p : 0.0f;
+        s[r] = p * (dp[r] - dl);                    // dS^T
       }
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        const bf16x8 sb0 = acc_to_b(s[0], hf), sb1 = acc_to_b(s[1], hf);
+        const bf16x8 sb = acc_to_b(s, hf);
 #pragma unroll
-        for (int t = 0; t < C::DT; ++t) {
-          const bf16x8 kf = frag_tr<DH>(kt, 32 * mt + 16 * hf, 32 * t, lane);
-          mfma_agpr(acc[0][t], kf, sb0);
-          mfma_agpr(acc[1][t], kf, sb1);
-          __builtin_amdgcn_sched_barrier(0);
-        }
+        for (int t = 0; t < C::DT; ++t)
+          acc[t] = mfma32x32x16(frag_tr<DH>(kt, 32 * mt + 16 * hf, 32 * t, lane), sb, acc[t]);
       }
     }
   };
 
   // Key tiles every query of the workgroup fully sees take the unmasked body; the
   // diagonal and ragged tiles (and every tile of a block with queries past the end)
-  // take the masked one. Every barrier is reached by all waves.
+  // take the masked one. Every barrier is reached by all waves; a wave skips the
+  // arithmetic of tiles entirely after its queries.
   int n_full = a.causal ? std::min(ntiles, (q0 + 1) / 64) : ntiles;
   n_full = std::min(n_full, S / 64);
   if (q0 + C::QROWS > S) n_full = 0;
@@ -143,25 +127,18 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
   }
   for (; j < ntiles; ++j) {
     step(j);
-    if (!(a.causal && 64 * j > qw + 63)) tile(j, std::true_type{});
+    if (!(a.causal && 64 * j > qw + 31)) tile(j, std::true_type{});
   }
 
+  if (qrow < a.Sp) {
+    bf16* dQt = (bf16*)a.dqt + (int64_t)h * DH * a.ld_dt + (int64_t)b * a.Sp + qrow;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) drain_all<C::DT>(acc[qb]);
+    for (int t = 0; t < C::DT; ++t)
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const int qrow = qw + 32 * qb + (lane & 31);
-    if (qrow < a.Sp) {
-      const bool qok = qrow < S;
-      bf16* dQt = (bf16*)a.dqt + (int64_t)h * DH * a.ld_dt + (int64_t)b * a.Sp + qrow;
-#pragma unroll
-      for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int d = 32 * t + acc_row(r, lane);
-          dQt[(int64_t)d * a.ld_dt] = (bf16)(qok ? acc[qb][t][r] * scale : 0.0f);
-        }
-    }
+      for (int r = 0; r < 16; ++r) {
+        const int d = 32 * t + acc_row(r, lane);
+        dQt[(int64_t)d * a.ld_dt] = (bf16)(qok ? acc[t][r] * scale : 0.0f);
+      }
   }
 }
 
@@ -231,7 +208,7 @@ static hipError_t dq_launch(Dt dt, const AttnArgs& a, hipStream_t s) {
     hipError_t e = set_lds(k, DqCfg<DH>::LDS);
     if (e != hipSuccess) return e;
     const int64_t nblk = (a.S + DqCfg<DH>::QROWS - 1) / DqCfg<DH>::QROWS;
-    hipLaunchKernelGGL(k, dim3((unsigned)(nblk * a.H * a.B)), dim3(256), DqCfg<DH>::LDS, s, a);
+    hipLaunchKernelGGL(k, dim3((unsigned)(nblk * a.H * a.B)), dim3(64 * DqCfg<DH>::NW), DqCfg<DH>::LDS, s, a);
   } else {
     const int lds = (2 * DH * 65 + 2 * 16 * DH) * 4;
     hipError_t e = set_lds(attn_bwd_dq_f32_kernel<DH>, lds);

@@ -181,27 +181,42 @@ __global__ __launch_bounds__(256) void row_sum_kernel(const T* in, int64_t ld, i
 }
 
 // ------------------------------------------------------------------ softmax-backward Delta
+// One wave per token (b, s): Delta[b, h, s] = sum_d dO[t, h*dh + d] O[t, h*dh + d] for every
+// head, from 16-byte loads of the token's two rows; the lanes of one head reduce by
+// shuffles. Also lse2 = lse * log2(e). Padding tokens s in [S, Sp) get zeros.
 template <typename T>
 __global__ __launch_bounds__(256) void delta_kernel(const T* dO, const T* O, int64_t ld, const float* lse,
                                                     float* delta, float* lse2, int B, int64_t S, int64_t Sp,
                                                     int H, int dh) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;     // over B * H * Sp
-  if (i >= (int64_t)B * H * Sp) return;
-  const int64_t s = i % Sp;
-  const int64_t bh = i / Sp;
-  const int h = (int)(bh % H), b = (int)(bh / H);
-  float acc = 0.0f;
-  if (s < S) {
-    const int64_t off = (b * S + s) * ld + (int64_t)h * dh;
-    for (int d = 0; d < dh; d += 4) {
-      float x[4], y[4];
-      Vec4<T>::load(dO + off + d, x);
-      Vec4<T>::load(O + off + d, y);
-      acc += (x[0] * y[0] + x[1] * y[1]) + (x[2] * y[2] + x[3] * y[3]);
+  constexpr int EPL = 16 / sizeof(T);                // elements per lane and load
+  const int lane = threadIdx.x & 63;
+  const int64_t tok = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);   // over B * Sp
+  if (tok >= (int64_t)B * Sp) return;
+  const int b = (int)(tok / Sp);
+  const int64_t s = tok % Sp;
+  const int D = H * dh, lpg = dh / EPL;             // lanes per head in one load step
+  for (int e0 = 0; e0 < D; e0 += 64 * EPL) {
+    const int e = e0 + lane * EPL;                  // the lanes of one head are all in or all out
+    float acc = 0.0f;
+    if (s < S && e < D) {
+      const int64_t off = ((int64_t)b * S + s) * ld + e;
+      float x[EPL], y[EPL];
+#pragma unroll
+      for (int k = 0; k < EPL; k += 4) {
+        Vec4<T>::load(dO + off + k, x + k);
+        Vec4<T>::load(O + off + k, y + k);
+      }
+#pragma unroll
+      for (int k = 0; k < EPL; ++k) acc = fmaf(x[k], y[k], acc);
+    }
+    for (int o = lpg / 2; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, 64);
+    if (lane % lpg == 0 && e < D) {
+      const int h = e / dh;
+      const int64_t i = ((int64_t)b * H + h) * Sp + s;
+      delta[i] = acc;
+      lse2[i] = s < S ? lse[i] * 1.4426950408889634f : 0.0f;
     }
   }
-  delta[i] = acc;
-  lse2[i] = s < S ? lse[i] * 1.4426950408889634f : 0.0f;
 }
 
 // ------------------------------------------------------------------ transpose / copy
@@ -306,8 +321,10 @@ hipError_t row_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols,
 
 hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, const float* lse, float* delta,
                       float* lse2, int B, int64_t S, int64_t Sp, int H, int dh, hipStream_t s) {
-  const int64_t n = (int64_t)B * H * Sp;
-  BPT_T(t, T, hipLaunchKernelGGL((delta_kernel<T>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+  // one wave per token; a head spans whole 16-byte loads
+  const int64_t n = (int64_t)B * Sp;
+  if (dh % (t == F32 ? 4 : 8) != 0) return hipErrorInvalidValue;
+  BPT_T(t, T, hipLaunchKernelGGL((delta_kernel<T>), dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s,
                                  (const T*)dout, (const T*)o, ld, lse, delta, lse2, B, S, Sp, H, dh));
   return hipGetLastError();
 }
