@@ -99,7 +99,15 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     }
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
+      // dP starts from -Delta of its query rows, so the MFMAs leave dP - Delta
+      f32x16 ndl;
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const f32x4 d4 = *(const f32x4*)(ls + 64 + 32 * mt + 8 * rg + 4 * (lane >> 5));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ndl[4 * rg + e] = -d4[e];
+      }
+      f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {ndl, ndl};
 #pragma unroll
       for (int kk = 0; kk < C::KSTEPS; ++kk) {
         const bf16x8 aq = frag_rows<DH>(qs, 32 * mt, 2 * kk, lane);
@@ -115,7 +123,6 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
       for (int rg = 0; rg < 4; ++rg) {
         const int qi = 32 * mt + 8 * rg + 4 * (lane >> 5);
         const f32x4 l4 = *(const f32x4*)(ls + qi);
-        const f32x4 d4 = *(const f32x4*)(ls + 64 + qi);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * rg + e;
@@ -127,7 +134,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
               p = (off >= lo[kb] && off <= hi[kb]) ? p : 0.0f;
             }
             s[kb][r] = p;
-            dp[kb][r] = p * (dp[kb][r] - d4[e]);       // dS
+            dp[kb][r] = p * dp[kb][r];                 // dS
           }
         }
         __builtin_amdgcn_sched_barrier(0);

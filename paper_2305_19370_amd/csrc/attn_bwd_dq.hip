@@ -79,7 +79,9 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
     const char* vt = kt + C::TB;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      f32x16 s = f32x16{}, dp = f32x16{};
+      f32x16 s = f32x16{}, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dp[r] = -dl;     // the MFMAs leave dP^T - Delta
 #pragma unroll
       for (int kk = 0; kk < C::KSTEPS; ++kk) {
         s = mfma32x32x16(frag_rows<DH>(kt, 32 * mt, 2 * kk, lane), qf[kk], s);
@@ -90,7 +92,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
       for (int r = 0; r < 16; ++r) {
         float p = fast_exp2(fmaf(s[r], c, nlse2));
         if constexpr (decltype(MASK)::value) p = (acc_row(r, lane) <= lim) ? p : 0.0f;
-        s[r] = p * (dp[r] - dl);                    // dS^T
+        s[r] = p * dp[r];                           // dS^T
       }
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
