@@ -6,26 +6,27 @@
 namespace bpt {
 
 // ====================================================================== backward dK dV, bf16
-// Key-outer: each wave owns 64 keys (two blocks of 32) and loops over query tiles of
-// 64 (two halves of 32). S = Q K^T and dP = dO V^T have the key on the lane axis, so
-// P and dS feed dV^T += dO^T P and dK^T += Q^T dS directly as B operands; dO^T and
-// Q^T fragments come from the token-major tiles by transposing LDS reads. Every
-// fragment read from LDS feeds the MFMAs of both key blocks.
+// Key-outer: 8 waves (two per SIMD, so one wave's VALU work overlaps the other's
+// MFMAs) of 32 keys each, 256 keys per workgroup, loop over query tiles of 64 (two
+// halves of 32). S = Q K^T and dP = dO V^T have the key on the lane axis, so P and dS
+// feed dV^T += dO^T P and dK^T += Q^T dS directly as B operands; dO^T and Q^T
+// fragments come from the token-major tiles by transposing LDS reads.
 // Query tiles are visited from the last one down, so all workgroups of a head start
 // on the same tiles (and share them in L2); the diagonal tiles come last.
 template <int DH>
 struct DkvCfg {
   static constexpr int KSTEPS = DH / 16, DT = DH / 32;
-  static constexpr int KEYS = 256;                  // keys per workgroup (4 waves x 64)
+  static constexpr int NW = 8;                      // waves per workgroup
+  static constexpr int KEYS = 32 * NW;              // keys per workgroup
   static constexpr int TB = RmTile<DH>::BYTES;
   static constexpr int STAGE = 2 * TB + 2 * 64 * 4; // Q, dO tiles; lse (base 2), delta
   static constexpr int NS = 4;                      // stages in the ring
   static constexpr int LDS = NS * STAGE;
-  static constexpr int DPS = Ring2<DH>::DPW + 2;    // copies per wave per stage
+  static constexpr int DPS = Ring2<DH, NW>::DPW + 2;  // copies per wave per stage
 };
 
 template <int DH>
-__global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) {
+__global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) {
   using C = DkvCfg<DH>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -36,7 +37,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
   xcd_map((int)blockIdx.x, nblk, a.H * a.B, hh, blk);
   const int h = hh % a.H, b = hh / a.H;
   const int k0 = blk * C::KEYS;                     // causal: low key blocks have the most queries
-  const int kw = k0 + 64 * wave;                    // first key of this wave
+  const int kw = k0 + 32 * wave;                    // first key of this wave
+  const int key = kw + (lane & 31);
   const float scale = rsqrtf((float)DH);
   const float c = scale * LOG2E;
 
@@ -47,16 +49,15 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
   const float* lse2 = a.lse2 + ((int64_t)b * a.H + h) * a.Sp;
   const float* delta = a.delta + ((int64_t)b * a.H + h) * a.Sp;
 
-  bf16x8 kf[2][C::KSTEPS], vf[2][C::KSTEPS];
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
-    const int key = kw + 32 * kb + (lane & 31), kr = key < S ? key : S - 1;
+  bf16x8 kf[C::KSTEPS], vf[C::KSTEPS];
+  {
+    const int kr = key < S ? key : S - 1;
 #pragma unroll
     for (int kk = 0; kk < C::KSTEPS; ++kk) {
-      kf[kb][kk] = __builtin_bit_cast(bf16x8, ld16(Kb + (int64_t)kr * a.ld_k + 16 * kk + 8 * (lane >> 5)));
-      vf[kb][kk] = __builtin_bit_cast(bf16x8, ld16(Vb + (int64_t)kr * a.ld_v + 16 * kk + 8 * (lane >> 5)));
-      settle(kf[kb][kk]);
-      settle(vf[kb][kk]);
+      kf[kk] = __builtin_bit_cast(bf16x8, ld16(Kb + (int64_t)kr * a.ld_k + 16 * kk + 8 * (lane >> 5)));
+      vf[kk] = __builtin_bit_cast(bf16x8, ld16(Vb + (int64_t)kr * a.ld_v + 16 * kk + 8 * (lane >> 5)));
+      settle(kf[kk]);
+      settle(vf[kk]);
     }
   }
 
@@ -67,21 +68,16 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
   auto issue = [&](int it) {
     const int qt0 = qstart + 64 * (ntiles - 1 - it);
     char* st = smem + (it % C::NS) * C::STAGE;
-    ring_issue<DH>(st, Qb, (int)a.ld_q, dOb, (int)a.ld_do, qt0, S - 1, wave, lane);
+    ring_issue<DH, C::NW>(st, Qb, (int)a.ld_q, dOb, (int)a.ld_do, qt0, S - 1, wave, lane);
     // base-2 lse and delta of the 64 queries (indices < Sp: in bounds; rows >= S are
     // masked); every wave copies them, so that all waves count the same copies
     dma4s(lse2 + qt0, 4u * lane, st + 2 * C::TB);
     dma4s(delta + qt0, 4u * lane, st + 2 * C::TB + 256);
   };
 
-  f32x16 adv[2][C::DT], adk[2][C::DT];
+  f32x16 adv[C::DT], adk[C::DT];
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int t = 0; t < C::DT; ++t) {
-      mfma_agpr_zero(adv[kb][t]);
-      mfma_agpr_zero(adk[kb][t]);
-    }
+  for (int t = 0; t < C::DT; ++t) adv[t] = adk[t] = f32x16{};
 
   auto tile = [&](int it, auto MASK) {
     const int qt0 = qstart + 64 * (ntiles - 1 - it);
@@ -89,34 +85,24 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     const char* ds = qs + C::TB;
     const float* ls = (const float*)(qs + 2 * C::TB);
     // query offset inside the tile of register r: 32*mt + acc_row(r, lane); visible
-    // for key block kb iff lo[kb] <= offset <= hi[kb]
-    int lo[2], hi[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const int key = kw + 32 * kb + (lane & 31);
-      lo[kb] = a.causal ? key - qt0 : 0;
-      hi[kb] = key < S ? S - 1 - qt0 : -1;
-    }
+    // iff lo <= offset <= hi
+    const int lo = a.causal ? key - qt0 : 0;
+    const int hi = key < S ? S - 1 - qt0 : -1;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
       // dP starts from -Delta of its query rows, so the MFMAs leave dP - Delta
-      f32x16 ndl;
+      f32x16 dp;
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
         const f32x4 d4 = *(const f32x4*)(ls + 64 + 32 * mt + 8 * rg + 4 * (lane >> 5));
 #pragma unroll
-        for (int e = 0; e < 4; ++e) ndl[4 * rg + e] = -d4[e];
+        for (int e = 0; e < 4; ++e) dp[4 * rg + e] = -d4[e];
       }
-      f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {ndl, ndl};
+      f32x16 s = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < C::KSTEPS; ++kk) {
-        const bf16x8 aq = frag_rows<DH>(qs, 32 * mt, 2 * kk, lane);
-        const bf16x8 ad = frag_rows<DH>(ds, 32 * mt, 2 * kk, lane);
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          s[kb] = mfma32x32x16(aq, kf[kb][kk], s[kb]);
-          dp[kb] = mfma32x32x16(ad, vf[kb][kk], dp[kb]);
-        }
+        s = mfma32x32x16(frag_rows<DH>(qs, 32 * mt, 2 * kk, lane), kf[kk], s);
+        dp = mfma32x32x16(frag_rows<DH>(ds, 32 * mt, 2 * kk, lane), vf[kk], dp);
         __builtin_amdgcn_sched_barrier(0);        // bound the fragments read ahead
       }
 #pragma unroll
@@ -126,31 +112,19 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * rg + e;
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb) {
-            float p = fast_exp2(fmaf(s[kb][r], c, -l4[e]));
-            if constexpr (decltype(MASK)::value) {
-              const int off = qi + e;
-              p = (off >= lo[kb] && off <= hi[kb]) ? p : 0.0f;
-            }
-            s[kb][r] = p;
-            dp[kb][r] = p * dp[kb][r];                 // dS
-          }
+          float p = fast_exp2(fmaf(s[r], c, -l4[e]));
+          if constexpr (decltype(MASK)::value) p = (qi + e >= lo && qi + e <= hi) ? p : 0.0f;
+          s[r] = p;
+          dp[r] = p * dp[r];                           // dS
         }
-        __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        const bf16x8 pb0 = acc_to_b(s[0], hf), pb1 = acc_to_b(s[1], hf);
-        const bf16x8 sb0 = acc_to_b(dp[0], hf), sb1 = acc_to_b(dp[1], hf);
+        const bf16x8 pb = acc_to_b(s, hf), sb = acc_to_b(dp, hf);
 #pragma unroll
         for (int t = 0; t < C::DT; ++t) {
-          const bf16x8 ado = frag_tr<DH>(ds, 32 * mt + 16 * hf, 32 * t, lane);
-          mfma_agpr(adv[0][t], ado, pb0);
-          mfma_agpr(adv[1][t], ado, pb1);
-          const bf16x8 aqt = frag_tr<DH>(qs, 32 * mt + 16 * hf, 32 * t, lane);
-          mfma_agpr(adk[0][t], aqt, sb0);
-          mfma_agpr(adk[1][t], aqt, sb1);
+          adv[t] = mfma32x32x16(frag_tr<DH>(ds, 32 * mt + 16 * hf, 32 * t, lane), pb, adv[t]);
+          adk[t] = mfma32x32x16(frag_tr<DH>(qs, 32 * mt + 16 * hf, 32 * t, lane), sb, adk[t]);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -190,27 +164,18 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     if (visible(it)) tile(it, std::true_type{});
   }
 
+  if (key < a.Sp) {
+    const int64_t col = (int64_t)b * a.Sp + key;
+    bf16* dKt = (bf16*)a.dkt + (int64_t)h * DH * a.ld_dt + col;
+    bf16* dVt = (bf16*)a.dvt + (int64_t)h * DH * a.ld_dt + col;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
-    drain_all<C::DT>(adv[kb]);
-    drain_all<C::DT>(adk[kb]);
-  }
+    for (int t = 0; t < C::DT; ++t)
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
-    const int key = kw + 32 * kb + (lane & 31);
-    if (key < a.Sp) {
-      const int64_t col = (int64_t)b * a.Sp + key;
-      bf16* dKt = (bf16*)a.dkt + (int64_t)h * DH * a.ld_dt + col;
-      bf16* dVt = (bf16*)a.dvt + (int64_t)h * DH * a.ld_dt + col;
-#pragma unroll
-      for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int64_t d = 32 * t + acc_row(r, lane);
-          dKt[d * a.ld_dt] = (bf16)(adk[kb][t][r] * scale);
-          dVt[d * a.ld_dt] = (bf16)adv[kb][t][r];
-        }
-    }
+      for (int r = 0; r < 16; ++r) {
+        const int64_t d = 32 * t + acc_row(r, lane);
+        dKt[d * a.ld_dt] = (bf16)(adk[t][r] * scale);
+        dVt[d * a.ld_dt] = (bf16)adv[t][r];
+      }
   }
 }
 
@@ -293,7 +258,7 @@ static hipError_t dkdv_launch(Dt dt, const AttnArgs& a, hipStream_t s) {
     hipError_t e = set_lds(k, DkvCfg<DH>::LDS);
     if (e != hipSuccess) return e;
     const int64_t nblk = (a.S + DkvCfg<DH>::KEYS - 1) / DkvCfg<DH>::KEYS;
-    hipLaunchKernelGGL(k, dim3((unsigned)(nblk * a.H * a.B)), dim3(256), DkvCfg<DH>::LDS, s, a);
+    hipLaunchKernelGGL(k, dim3((unsigned)(nblk * a.H * a.B)), dim3(64 * DkvCfg<DH>::NW), DkvCfg<DH>::LDS, s, a);
   } else {
     const int lds = (2 * DH * 65 + 2 * 16 * DH + 32) * 4;
     hipError_t e = set_lds(attn_bwd_dkdv_f32_kernel<DH>, lds);
