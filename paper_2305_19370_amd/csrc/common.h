@@ -41,8 +41,28 @@ BPT_DEV float warp_sum(float v) {
   return v;
 }
 
-BPT_DEV float gelu_f(float z) { return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f)); }
+// GELU with the exact erf, in fp32. erf of |z|/sqrt(2) by Abramowitz & Stegun,
+// Handbook of Mathematical Functions, eq. 7.1.26: erf(x) = 1 - t P(t) exp(-x^2) with
+// t = 1 / (1 + p x) and a degree-5 polynomial, |error| <= 1.5e-7 for x >= 0. The
+// exp(-z^2/2) it needs is also the normal density of GELU' = Phi(z) + z phi(z).
+BPT_DEV void gelu_both(float z, float& g, float& gp) {
+  const float x = fabsf(z) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
+  const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f),
+                                      -0.284496736f), 0.254829592f);
+  const float e = __builtin_amdgcn_exp2f(-x * x * 1.4426950408889634f);   // exp(-z^2 / 2)
+  const float erf_abs = fmaf(-poly, e, 1.0f);
+  const float phi_cdf = 0.5f + 0.5f * copysignf(erf_abs, z);            // Phi(z)
+  g = z * phi_cdf;
+  gp = fmaf(z * 0.39894228040143268f, e, phi_cdf);                       // + z exp(-z^2/2) / sqrt(2 pi)
+}
+BPT_DEV float gelu_f(float z) {
+  float g, gp;
+  gelu_both(z, g, gp);
+  return g;
+}
 BPT_DEV float gelu_grad_f(float z) {
-  return 0.5f * (1.0f + erff(z * 0.70710678118654752f)) +
-         z * 0.39894228040143268f * __expf(-0.5f * z * z);
+  float g, gp;
+  gelu_both(z, g, gp);
+  return gp;
 }

@@ -85,18 +85,51 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
       if (a.bias_on_m) v += a.bias[m];
       else v += *(const f32x4*)(a.bias + n);
     }
-    if (a.C2) {
-      f32x4 d;
+    f32x4 d;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) d[e] = gelu_grad_f(v[e]);
-      *(f32x4*)(a.C2 + z * a.sC2 + m * a.ldc2 + n) = d;
+    for (int e = 0; e < 4; ++e) {
+      float g, gp;
+      gelu_both(v[e], g, gp);
+      v[e] = g;
+      d[e] = gp;
     }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = gelu_f(v[e]);
+    if (a.C2) *(f32x4*)(a.C2 + z * a.sC2 + m * a.ldc2 + n) = d;
   } else {
     v *= *(const f32x4*)((const float*)a.R + z * a.sR + m * a.ldr + n);
   }
   V4<CT>::st(C, v);
+}
+
+// Four consecutive columns n..n+3 of row m inside the stored width, from pointers
+// already at (m, n): c into C, r into R (EPI_RESID / EPI_MUL), c2 into C2 (EPI_GELU),
+// bn at bias[n]; bm = bias[m] for a per-row bias.
+template <int EPI, typename CT, typename RT>
+BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, float* c2, const float* bn, float bm, f32x4 v) {
+  if constexpr (EPI == EPI_STORE) {
+    if constexpr (sizeof(CT) == 4) {
+      if (a.accumulate) v += V4<CT>::ld(c);
+    }
+  } else if constexpr (EPI == EPI_RESID) {
+    v += V4<RT>::ld((const RT*)r);
+    if (a.bias) v += *(const f32x4*)bn;
+  } else if constexpr (EPI == EPI_GELU) {
+    if (a.bias) {
+      if (a.bias_on_m) v += bm;
+      else v += *(const f32x4*)bn;
+    }
+    f32x4 d;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float g, gp;
+      gelu_both(v[e], g, gp);
+      v[e] = g;
+      d[e] = gp;
+    }
+    if (a.C2) *(f32x4*)c2 = d;
+  } else {
+    v *= *(const f32x4*)r;
+  }
+  V4<CT>::st(c, v);
 }
 
 // ------------------------------------------------------------------ bf16 MFMA kernel
@@ -294,11 +327,14 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
   }
   __syncthreads();
 
-  // Epilogue: each wave stages one 32-row strip of its accumulators in LDS (free
-  // after the K loop), then every lane applies the epilogue to groups of 4
-  // consecutive columns and stores them with one vector store.
+  // Epilogue: each wave stages one 32-row strip of its accumulators in its own part of
+  // the (now idle) LDS, then every lane applies the epilogue to groups of 4 consecutive
+  // columns and stores them with one vector store. The strips are private to their
+  // wave, so no barrier is needed between strips.
   constexpr int PITCHF = Cfg::WN + 4;                // floats per staged row
+  constexpr int C4 = Cfg::WN / 4;                    // 4-column groups per row
   float* strip = (float*)smem + wave * 32 * PITCHF;
+  const bool inside = m0 + BM <= a.M && n0 + BN <= a.N;
 #pragma unroll
   for (int i = 0; i < Cfg::TM; ++i) {
 #pragma unroll
@@ -306,18 +342,41 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         strip[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * PITCHF + 32 * j + (lane & 31)] = acc[i][j][r];
-    __syncthreads();
+    const int64_t mrow = m0 + wm * Cfg::WM + 32 * i;
+    const int64_t ncol = n0 + wn * Cfg::WN;
+    if (inside) {
+      // rows are (lane / C4) + (64 / C4) * it; columns 4 * (lane % C4)
+      const int r0 = lane / C4, c0 = 4 * (lane % C4);
+      CT* cb = (CT*)a.C + z * a.sC + (mrow + r0) * a.ldc + ncol + c0;
+      const char* rb = nullptr;
+      if constexpr (EPI == EPI_RESID) rb = (const char*)((const RT*)a.R + z * a.sR + (mrow + r0) * a.ldr + ncol + c0);
+      else if constexpr (EPI == EPI_MUL) rb = (const char*)((const float*)a.R + z * a.sR + (mrow + r0) * a.ldr + ncol + c0);
+      float* c2b = (EPI == EPI_GELU && a.C2) ? a.C2 + z * a.sC2 + (mrow + r0) * a.ldc2 + ncol + c0 : nullptr;
+      const float* bb = a.bias ? a.bias + ncol + c0 : nullptr;
+      constexpr int RS = EPI == EPI_MUL ? 4 : (int)sizeof(RT);
+      constexpr int RSTEP = 64 / C4;                 // rows per iteration
+      // the GELU epilogue is long: keep its loop rolled (instruction cache)
+      constexpr int UNR = EPI == EPI_GELU ? 4 : 32 / RSTEP;
+#pragma unroll UNR
+      for (int it = 0; it < 32 / RSTEP; ++it) {
+        const int row = r0 + RSTEP * it;
+        const f32x4 v = *(const f32x4*)(strip + row * PITCHF + c0);
+        const float bm = (EPI == EPI_GELU && a.bias && a.bias_on_m) ? a.bias[mrow + row] : 0.0f;
+        epi_vec4<EPI, CT, RT>(a, cb + (int64_t)RSTEP * it * a.ldc,
+                              rb + (int64_t)RSTEP * it * a.ldr * RS,
+                              c2b + (int64_t)RSTEP * it * a.ldc2, bb, bm, v);
+      }
+    } else {
 #pragma unroll 1
-    for (int e = lane; e < 32 * Cfg::WN / 4; e += 64) {
-      const int row = e / (Cfg::WN / 4), c4 = e % (Cfg::WN / 4);
-      const int64_t m = m0 + wm * Cfg::WM + 32 * i + row;
-      const int64_t n = n0 + wn * Cfg::WN + 4 * c4;
-      if (m < a.M && n < ncols) {
-        const f32x4 v = *(const f32x4*)(strip + row * PITCHF + 4 * c4);
-        epi_store4<EPI, CT, RT>(a, z, m, n, ncols, v);
+      for (int e = lane; e < 32 * C4; e += 64) {
+        const int row = e / C4, c4 = e % C4;
+        const int64_t m = mrow + row, n = ncol + 4 * c4;
+        if (m < a.M && n < ncols) {
+          const f32x4 v = *(const f32x4*)(strip + row * PITCHF + 4 * c4);
+          epi_store4<EPI, CT, RT>(a, z, m, n, ncols, v);
+        }
       }
     }
-    __syncthreads();
   }
 }
 
