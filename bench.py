@@ -62,6 +62,60 @@ def cpu_baseline(w, sample_S: int):
             "seconds": dt}
 
 
+# Sources whose every byte defines a launch class's kernel: a recorded HBM-traffic
+# measurement of that class applies only while their hash is unchanged.
+TRAFFIC_SOURCES = {
+    cls: ["paper_2305_19370_amd/csrc/" + f, "paper_2305_19370_amd/csrc/attn_common.h",
+          "paper_2305_19370_amd/csrc/common.h", "paper_2305_19370_amd/csrc/internal.h",
+          "paper_2305_19370_amd/build.py"]
+    for cls, f in (("attn.bwd_dkdv", "attn_bwd_dkdv.hip"), ("attn.bwd_dq", "attn_bwd_dq.hip"),
+                   ("attn.fwd", "attn_fwd.hip"))
+}
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "attn_kernels_7b_s32768_hbm_traffic.md")
+
+
+def source_hash(cls: str):
+    import hashlib
+    if cls not in TRAFFIC_SOURCES:
+        return None
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES[cls]:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(cls: str, workload: str):
+    """HBM bytes per launch of a launch class, from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, calibrated on a plain copy), or None when there
+    is none for this class and workload or its kernel sources changed since."""
+    h = source_hash(cls)
+    if h is None or not os.path.exists(TRAFFIC_RECORD):
+        return None
+    with open(TRAFFIC_RECORD) as fh:
+        for line in fh:
+            # | class | workload | source hash | fetch bytes | write bytes | total bytes |
+            cells = [c.strip().strip("`") for c in line.strip().strip("|").split("|")]
+            if len(cells) == 6 and cells[0] == cls and cells[1] == workload and cells[2] == h:
+                return int(cells[5])
+    return None
+
+
+def copy_probe(nbytes: int, reps: int) -> int:
+    """A plain device copy of nbytes (read nbytes, write nbytes), the calibration
+    reference for the HBM byte counters."""
+    import torch
+    torch.cuda.set_device(0)
+    src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes, "reps": reps}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -70,7 +124,11 @@ def main() -> int:
     ap.add_argument("--workload", default="bf16_7b_s32768")
     ap.add_argument("--cpu-sample-s", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES (counter calibration)")
     args = ap.parse_args()
+    if args.copy_probe:
+        return copy_probe(args.copy_probe, 3)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
               "sharding of the layer is a design, not part of this build", file=sys.stderr)
@@ -155,7 +213,8 @@ def main() -> int:
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM_GBS}
     roof.update({"kernel": name, "launches_per_step": rec["count"] / args.steps,
-                 "avg_launch_ms": rec["ms"] / rec["count"], "traffic": None})
+                 "avg_launch_ms": rec["ms"] / rec["count"], "traffic": recorded_traffic(name, w.name),
+                 "traffic_unit": "bytes per launch"})
     breakdown = {k: {"ms_per_step": v["ms"] / args.steps,
                      "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["flops"] > 0 and v["ms"] > 0 else None,
                      "gbs": (v["bytes"] / (v["ms"] / 1e3) / 1e9) if v["ms"] > 0 else None}
