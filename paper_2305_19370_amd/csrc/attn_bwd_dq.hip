@@ -64,9 +64,11 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
 
   const int kv_end = a.causal ? (q0 + C::QROWS < S ? q0 + C::QROWS : S) : S;
   const int ntiles = (kv_end + 63) / 64;
+  const RingOff<DH, C::NW> roff = ring_offsets<DH, C::NW>((int)a.ld_k, (int)a.ld_v, wave, lane);
   auto issue = [&](int j) {
-    ring_issue<DH, C::NW>(smem + (j % C::NS) * C::STAGE, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, S - 1, wave,
-                          lane);
+    char* st = smem + (j % C::NS) * C::STAGE;
+    if (64 * j + 63 < S) ring_issue_full<DH, C::NW>(st, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, roff, wave);
+    else ring_issue<DH, C::NW>(st, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, S - 1, wave, lane);
   };
 
   f32x16 acc[C::DT];                                // dQ^T of the wave's queries

@@ -95,6 +95,41 @@ BPT_DEV void ring_issue(char* stage, const bf16* src0, int ld0, const bf16* src1
   }
 }
 
+// The per-lane byte offsets of ring_issue for a stage whose 64 rows all exist
+// (row0 + 63 <= last_row), computed once per kernel: they depend only on the lane,
+// the wave and the two row strides.
+template <int DH, int NW>
+struct RingOff {
+  uint32_t o[Ring2<DH, NW>::DPW];
+};
+
+template <int DH, int NW>
+BPT_DEV RingOff<DH, NW> ring_offsets(int ld0, int ld1, int wave, int lane) {
+  using T = RmTile<DH>;
+  RingOff<DH, NW> r;
+#pragma unroll
+  for (int i = 0; i < Ring2<DH, NW>::DPW; ++i) {
+    const int b = ring_block<DH, NW>(wave, i), t = b >= T::BLOCKS, blk = b - t * T::BLOCKS;
+    const int slot = blk * 64 + lane, col = slot % T::SLOTS, row = slot / T::SLOTS;
+    r.o[i] = 2u * (uint32_t)(row * (t ? ld1 : ld0) + (col < DH / 8 ? col : 0) * 8);
+  }
+  return r;
+}
+
+// ring_issue for a full stage with precomputed offsets.
+template <int DH, int NW>
+BPT_DEV void ring_issue_full(char* stage, const bf16* src0, int ld0, const bf16* src1, int ld1, int row0,
+                             const RingOff<DH, NW>& r, int wave) {
+  using T = RmTile<DH>;
+  const bf16* org0 = src0 + (int64_t)row0 * ld0;
+  const bf16* org1 = src1 + (int64_t)row0 * ld1;
+#pragma unroll
+  for (int i = 0; i < Ring2<DH, NW>::DPW; ++i) {
+    const int b = ring_block<DH, NW>(wave, i), t = b >= T::BLOCKS, blk = b - t * T::BLOCKS;
+    dma16s(t ? org1 : org0, r.o[i], stage + t * T::BYTES + blk * 1024);
+  }
+}
+
 // A-operand fragment with tile rows as MFMA rows: lane l reads row (row0 + l%32),
 // features 8*kc' .. 8*kc'+7 where kc' = kc + l/32 (kc even).
 template <int DH>
