@@ -2,14 +2,15 @@
 //
 // Every dense contraction of the layer (QKV / output projections, both FFN
 // linears and all their weight / input gradients) is issued in this one "NT"
-// form, with both operands contiguous along K; the host arranges layouts
-// (pre-transposed weights, feature-major activations) so that no kernel ever
-// needs a strided operand read.
+// form. Operands are normally contiguous along K; a plain-store GEMM may also take
+// either operand stored K-major (token-major activations contracted over tokens,
+// feature-major gradients contracted over features), which the kernel transposes
+// on its way from LDS into the MFMA registers.
 //
 // bf16 path: gfx950 MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation, 256 threads
-// (2 x 2 waves), K step 64 staged through double-buffered LDS with an XOR swizzle
-// of 16-byte chunks so that the 32 rows a fragment read touches fall in distinct
-// banks. fp32 path: plain VALU FMA tiles (used for the fp32 parity workload).
+// (2 x 2 waves), K step 32 per stage through an LDS ring with XOR-swizzled 16-byte
+// chunks, so that the rows a fragment read touches fall in distinct banks. fp32 path:
+// plain VALU FMA tiles (used for the fp32 parity workload).
 #include "common.h"
 #include "internal.h"
 #include <type_traits>
@@ -174,7 +175,39 @@ BPT_DEV int swz(int r) { return (((r >> 1) ^ (r >> 3)) & 1) | (r & 4) >> 1; }
 
 template <int N> BPT_DEV void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
-template <int BM, int BN, int EPI, typename CT, typename RT>
+// Operand tiles stored transposed (source rows are k, the M or N extent contiguous):
+// 32 rows of 2 * BX bytes per stage, chunk c of row k at chunk position c ^ 4 (k % 4).
+// A fragment (8 consecutive k of one column per lane) is two ds_read_b64_tr_b16: in each
+// group of 16 lanes, lane m addresses 4 columns of one row (row m / 4, columns 4 (m % 4)..)
+// and receives column m of the group's 4 rows. Over the 32 lanes the hardware serves
+// together (4 rows, 64 bytes each), the XOR places the rows in distinct 64-byte bank groups.
+template <int BX>
+struct TrTile {
+  static constexpr int RB = 2 * BX;                    // bytes per k row
+  static constexpr int CPR = RB / 16;                  // 16-byte chunks per row
+};
+
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short g_s16x4;
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short g_s16x8;
+BPT_DEV bf16x8 tr_frag(const char* p, int second) {
+  typedef __attribute__((address_space(3))) g_s16x4 lds_s16x4;
+  const g_s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+  const g_s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + second));
+  const g_s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// Per-lane source offset (elements) of copy slot `slot` of a transposed operand tile:
+// k row `row` of the tile, logical chunk from the swizzle, columns clamped to the readable
+// width (cols_left = readable columns from the tile's first column, >= 8).
+template <int BX>
+BPT_DEV void tr_slot(int slot, int& row, int& col, int cols_left) {
+  row = slot / TrTile<BX>::CPR;
+  const int lc = (slot % TrTile<BX>::CPR) ^ (4 * (row & 3));
+  col = 8 * lc < cols_left - 8 ? 8 * lc : cols_left - 8;
+}
+
+template <int BM, int BN, int EPI, typename CT, typename RT, bool TA = false, bool TB = false>
 __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
   using Cfg = TileCfg<BM, BN>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -199,9 +232,13 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
   const int tm = first_m + (pid % (GM * tiles_n)) % gm;
   const int tn = (pid % (GM * tiles_n)) / gm;
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN, z = blockIdx.z;
-  const bf16* A = (const bf16*)a.A + z * a.sA + m0 * a.lda;
-  const bf16* B = (const bf16*)a.B + z * a.sB + n0 * a.ldb;
+  const bf16* A = (const bf16*)a.A + z * a.sA + (TA ? m0 : m0 * a.lda);
+  const bf16* B = (const bf16*)a.B + z * a.sB + (TB ? n0 : n0 * a.ldb);
   const int nk = (int)(a.K / Cfg::BK);
+  // transposed operands: readable k rows and columns (from the tile's first column)
+  const int64_t arows = a.a_rows > 0 ? a.a_rows : a.K, brows = a.b_rows > 0 ? a.b_rows : a.K;
+  const int acols = (int)((a.a_cols > 0 ? a.a_cols : a.M) - m0);
+  const int bcols = (int)((a.b_cols > 0 ? a.b_cols : a.N) - n0);
 
   // per-lane source offsets (elements) of this wave's copy slots; rows past the
   // matrix edge are clamped to its last row (their results are never stored)
@@ -212,32 +249,65 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
     for (int i = 0; i < Cfg::APW; ++i) {
       int blk = wave + 4 * i;
       blk = blk < Cfg::ABLK ? blk : Cfg::ABLK - 1;     // extra copies repeat the last block
-      const int slot = blk * 64 + lane, row = slot >> 2, col = (slot & 3) ^ swz(row);
-      aoff[i] = (row < alast ? row : alast) * (int)a.lda + col * 8;
+      const int slot = blk * 64 + lane;
+      if constexpr (TA) {
+        int row, col;
+        tr_slot<BM>(slot, row, col, acols);
+        aoff[i] = row * (int)a.lda + col;
+      } else {
+        const int row = slot >> 2, col = (slot & 3) ^ swz(row);
+        aoff[i] = (row < alast ? row : alast) * (int)a.lda + col * 8;
+      }
     }
 #pragma unroll
     for (int i = 0; i < Cfg::BPW; ++i) {
       int blk = wave + 4 * i;
       blk = blk < Cfg::BBLK ? blk : Cfg::BBLK - 1;
-      const int slot = blk * 64 + lane, row = slot >> 2, col = (slot & 3) ^ swz(row);
-      boff[i] = (row < blast ? row : blast) * (int)a.ldb + col * 8;
+      const int slot = blk * 64 + lane;
+      if constexpr (TB) {
+        int row, col;
+        tr_slot<BN>(slot, row, col, bcols);
+        boff[i] = row * (int)a.ldb + col;
+      } else {
+        const int row = slot >> 2, col = (slot & 3) ^ swz(row);
+        boff[i] = (row < blast ? row : blast) * (int)a.ldb + col * 8;
+      }
     }
   }
   // copy d (0 <= d < DPS) of this wave for stage kt: A blocks first, then B blocks
   // LDS address of the tile ring (the copies take LDS addresses, not generic pointers)
   const uint32_t ring = __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem);
+  // A transposed operand's stage is k rows k0 .. k0+31; rows from x_rows on are clamped to
+  // the last readable row (the caller guarantees the other operand is zero there).
+  auto tr_src = [&](const bf16* X, int64_t ld, int64_t xrows, int cols, int k0, int blk, int off,
+                    auto BXc) -> const bf16* {
+    constexpr int BX = decltype(BXc)::value;
+    if (k0 + Cfg::BK <= xrows) return X + (int64_t)k0 * ld + off;
+    int row, col;
+    tr_slot<BX>(blk * 64 + lane, row, col, cols);
+    const int64_t r = k0 + row < xrows ? k0 + row : xrows - 1;
+    return X + r * ld + col;
+  };
   auto dma = [&](int kt, int d) {
     const uint32_t st = ring + (kt % Cfg::NS) * Cfg::STAGE;
     const int k0 = kt * Cfg::BK;
     if (d < Cfg::APW) {
       int blk = wave + 4 * d;
       blk = blk < Cfg::ABLK ? blk : Cfg::ABLK - 1;
-      lds_dma16(A + k0 + aoff[d], st + blk * 1024);
+      if constexpr (TA)
+        lds_dma16(tr_src(A, a.lda, arows, acols, k0, blk, aoff[d], std::integral_constant<int, BM>{}),
+                  st + blk * 1024);
+      else
+        lds_dma16(A + k0 + aoff[d], st + blk * 1024);
     } else {
       int blk = wave + 4 * (d - Cfg::APW);
       blk = blk < Cfg::BBLK ? blk : Cfg::BBLK - 1;
-      lds_dma16(B + k0 + boff[d - Cfg::APW], st + Cfg::ABYTES + blk * 1024);
+      if constexpr (TB)
+        lds_dma16(tr_src(B, a.ldb, brows, bcols, k0, blk, boff[d - Cfg::APW], std::integral_constant<int, BN>{}),
+                  st + Cfg::ABYTES + blk * 1024);
+      else
+        lds_dma16(B + k0 + boff[d - Cfg::APW], st + Cfg::ABYTES + blk * 1024);
     }
   };
 
@@ -256,11 +326,36 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
 
   // Fragments are double-buffered in registers. Fragment r of a k step (0: A0,
   // 1..TN: B0.., then A1..) is read in the order the MFMAs of the next k step use them.
+  // transposed tiles: per-lane byte offset of fragment i (32 columns) for k step 0; the
+  // second read of a fragment is 4 rows further, k step 1 16 rows further
+  int tra[Cfg::TM], trb[Cfg::TN];
+  {
+    const int g = lane >> 4, m = lane & 15, sx = (m >> 2) & 3, q = 2 * (g & 1) + ((m >> 1) & 1);
+    const int rowpart = 8 * (g >> 1) + (m >> 2), within = 16 * q + 8 * (m & 1);
+    if constexpr (TA) {
+#pragma unroll
+      for (int i = 0; i < Cfg::TM; ++i)
+        tra[i] = rowpart * TrTile<BM>::RB + 64 * (((wm * Cfg::WM) / 32 + i) ^ sx) + within;
+    }
+    if constexpr (TB) {
+#pragma unroll
+      for (int j = 0; j < Cfg::TN; ++j)
+        trb[j] = Cfg::ABYTES + rowpart * TrTile<BN>::RB + 64 * (((wn * Cfg::WN) / 32 + j) ^ sx) + within;
+    }
+  }
   bf16x8 fa[2][Cfg::TM], fb[2][Cfg::TN];
+  auto read_a = [&](const char* st, int kk, int buf, int i) {
+    if constexpr (TA) fa[buf][i] = tr_frag(st + tra[i] + kk * 16 * TrTile<BM>::RB, 4 * TrTile<BM>::RB);
+    else fa[buf][i] = *(const bf16x8*)(st + abase[kk] + i * 32 * Cfg::PITCH);
+  };
+  auto read_b = [&](const char* st, int kk, int buf, int j) {
+    if constexpr (TB) fb[buf][j] = tr_frag(st + trb[j] + kk * 16 * TrTile<BN>::RB, 4 * TrTile<BN>::RB);
+    else fb[buf][j] = *(const bf16x8*)(st + bbase[kk] + j * 32 * Cfg::PITCH);
+  };
   auto read_frag = [&](const char* st, int kk, int buf, int r) {
-    if (r == 0) fa[buf][0] = *(const bf16x8*)(st + abase[kk]);
-    else if (r <= Cfg::TN) fb[buf][r - 1] = *(const bf16x8*)(st + bbase[kk] + (r - 1) * 32 * Cfg::PITCH);
-    else fa[buf][r - Cfg::TN] = *(const bf16x8*)(st + abase[kk] + (r - Cfg::TN) * 32 * Cfg::PITCH);
+    if (r == 0) read_a(st, kk, buf, 0);
+    else if (r <= Cfg::TN) read_b(st, kk, buf, r - 1);
+    else read_a(st, kk, buf, r - Cfg::TN);
   };
   // One k step: the TM x TN MFMAs on fragment buffer CUR, each followed by at most one
   // fragment read of the next k step (stage rkt, half rkk) into the other buffer and by
@@ -391,12 +486,16 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   const float* B = (const float*)a.B + z * a.sB;
   float acc[4][4] = {};
   const int lr = tid >> 2, lk = (tid & 3) * 4;
+  const int64_t arows = a.trans_a && a.a_rows > 0 ? a.a_rows : a.K;
+  const int64_t brows = a.trans_b && a.b_rows > 0 ? a.b_rows : a.K;
   for (int64_t k0 = 0; k0 < a.K; k0 += 16) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int64_t k = k0 + lk + e;
-      As[lk + e][lr] = (m0 + lr < a.M && k < a.K) ? A[(m0 + lr) * a.lda + k] : 0.0f;
-      Bs[lk + e][lr] = (n0 + lr < a.N && k < a.K) ? B[(n0 + lr) * a.ldb + k] : 0.0f;
+      const int64_t ai = a.trans_a ? k * a.lda + m0 + lr : (m0 + lr) * a.lda + k;
+      const int64_t bi = a.trans_b ? k * a.ldb + n0 + lr : (n0 + lr) * a.ldb + k;
+      As[lk + e][lr] = (m0 + lr < a.M && k < arows) ? A[ai] : 0.0f;
+      Bs[lk + e][lr] = (n0 + lr < a.N && k < brows) ? B[bi] : 0.0f;
     }
     __syncthreads();
 #pragma unroll
@@ -424,10 +523,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 }
 
 // ------------------------------------------------------------------ dispatch
-template <int BM, int BN, int EPI, typename CT, typename RT>
+template <int BM, int BN, int EPI, typename CT, typename RT, bool TA = false, bool TB = false>
 static hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
   using Cfg = TileCfg<BM, BN>;
-  auto kern = gemm_bf16_kernel<BM, BN, EPI, CT, RT>;
+  auto kern = gemm_bf16_kernel<BM, BN, EPI, CT, RT, TA, TB>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -454,6 +553,24 @@ static hipError_t launch_typed(Dt ab, const GemmArgs& a, hipStream_t s) {
     return hipGetLastError();
   }
   const int64_t big = ((a.M + 255) / 256) * ((ncols + 255) / 256) * a.batch;
+  if (a.trans_a || a.trans_b) {
+    if constexpr (EPI == EPI_STORE) {
+      // a transposed operand is read in 16-byte column chunks
+      if ((a.trans_a && ((a.a_cols > 0 ? a.a_cols : a.M) % 8 || a.lda % 8)) ||
+          (a.trans_b && ((a.b_cols > 0 ? a.b_cols : a.N) % 8 || a.ldb % 8)))
+        return hipErrorInvalidValue;
+      if (a.trans_a && a.trans_b)
+        return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, true>(a, s)
+                          : launch_bf16<128, 128, EPI, CT, RT, true, true>(a, s);
+      if (a.trans_a)
+        return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, false>(a, s)
+                          : launch_bf16<128, 128, EPI, CT, RT, true, false>(a, s);
+      return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, false, true>(a, s)
+                        : launch_bf16<128, 128, EPI, CT, RT, false, true>(a, s);
+    } else {
+      return hipErrorInvalidValue;
+    }
+  }
   if (big >= 256) return launch_bf16<256, 256, EPI, CT, RT>(a, s);
   return launch_bf16<128, 128, EPI, CT, RT>(a, s);
 }

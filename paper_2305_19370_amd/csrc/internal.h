@@ -32,6 +32,14 @@ struct GemmArgs {
   int batch = 1;
   int accumulate = 0;          // fp32 C only: C += acc
   int bias_on_m = 0;           // EPI_GELU: bias indexed by row instead of column
+  // Transposed operands (EPI_STORE only): trans_a means A is stored K-major, element
+  // (m, k) at A[k * lda + m]; likewise trans_b for B (element (n, k) at B[k * ldb + n]).
+  // For such an operand, x_rows is the number of k rows that may be read (rows from
+  // x_rows up to K are not read, and the other operand must be zero at those k), and
+  // x_cols the number of columns that may be read from the pointer (>= M or N; a
+  // multiple of 8). 0 means K and M (or N).
+  int trans_a = 0, trans_b = 0;
+  int64_t a_rows = 0, b_rows = 0, a_cols = 0, b_cols = 0;
 };
 
 // ab: element type of A and B. ct: type of C; rt: type of R.

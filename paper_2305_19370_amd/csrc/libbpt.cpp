@@ -138,10 +138,10 @@ FwdWs fwd_ws(const Dims& d, void* base, int64_t* total) {
 
 struct BwdWs {
   void *w1T, *wcat;
-  void *vg, *vgT, *gT, *dzT, *dz, *dyT;
+  void *vg, *gT, *dzT;
   float* gpT;
   float *dv, *dh, *dU, *delta, *lse2, *partial, *scratch;
-  void *dhe, *dhT, *oT, *dO, *dqkvT, *dqkv, *u, *uT;
+  void *dhe, *dhT, *dO, *dqkvT, *u;
 };
 
 BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
@@ -150,24 +150,18 @@ BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
   w.w1T = bp.take(d.F * d.D * d.E);
   w.wcat = bp.take(3 * d.D * d.D * d.E);
   w.vg = bp.take(d.R * d.D * d.E);
-  w.vgT = bp.take(d.D * d.Rp * d.E);
   w.gT = bp.take(d.F * d.Rp * d.E);
   w.gpT = (float*)bp.take(d.F * d.Rp * 4);
   w.dzT = bp.take(d.F * d.Rp * d.E);
-  w.dz = bp.take(d.R * d.F * d.E);
-  w.dyT = bp.take(d.D * d.Rp * d.E);
   w.dv = (float*)bp.take(d.T * d.D * 4);
   w.dh = (float*)bp.take(d.T * d.D * 4);
   w.dhe = bp.take(d.T * d.D * d.E);
   w.dhT = bp.take(d.D * d.Tp * d.E);
-  w.oT = bp.take(d.D * d.Tp * d.E);
   w.dO = bp.take(d.T * d.D * d.E);
   w.delta = (float*)bp.take(d.B * d.H * d.Sp * 4);
   w.lse2 = (float*)bp.take(d.B * d.H * d.Sp * 4);
   w.dqkvT = bp.take(3 * d.D * d.Tp * d.E);
-  w.dqkv = bp.take(d.T * 3 * d.D * d.E);
   w.u = bp.take(d.T * d.D * d.E);
-  w.uT = bp.take(d.D * d.Tp * d.E);
   w.dU = (float*)bp.take(d.T * d.D * 4);
   w.partial = (float*)bp.take((int64_t)layer_norm_param_grad_ws(std::max(d.D, d.F)) * 4);
   w.scratch = (float*)bp.take(2 * std::max(d.D, d.F) * 4);
@@ -502,24 +496,23 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
         RUN("gemm.bwd_dz", gemm_flops(g), gemm_bytes(g, E_, E_ + 4), gemm(E, EPI_MUL, E, F32, g, s));
       }
       if (G.db1) RUN("reduce.bias", 0, (double)F * r * E_, row_sum(E, w.dzT, d.Rp, F, r, G.db1, first ? 0 : 1, s));
-      if (G.dW2) {   // dW2 = G^T dY
-        RUN("transpose.act", 0, tb * r * D, transpose(E, dYg, D, 0, w.dyT, d.Rp, 0, r, D, rp, 1, s));
+      if (G.dW2) {   // dW2 = G^T dY, dY read token-major (G^T is zero past the group's rows)
         GemmArgs g;
-        g.A = w.gT; g.lda = d.Rp; g.B = w.dyT; g.ldb = d.Rp; g.C = G.dW2; g.ldc = D;
-        g.M = F; g.N = D; g.K = rp; g.accumulate = first ? 0 : 1;
+        g.A = w.gT; g.lda = d.Rp; g.B = dYg; g.ldb = D; g.trans_b = 1; g.b_rows = r;
+        g.C = G.dW2; g.ldc = D; g.M = F; g.N = D; g.K = rp; g.accumulate = first ? 0 : 1;
         RUN("gemm.bwd_dw2", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
       }
-      RUN("transpose.act", 0, tb * r * F, transpose(E, w.dzT, d.Rp, 0, w.dz, F, 0, F, r, F, 1, s));
-      {   // dv = dZ W1^T
+      {   // dv = dZ W1^T, dZ read from its feature-major copy
         GemmArgs g;
-        g.A = w.dz; g.lda = F; g.B = p->W1; g.ldb = F; g.C = w.dv + t0 * D; g.ldc = D;
+        g.A = w.dzT; g.lda = d.Rp; g.trans_a = 1; g.a_cols = d.Rp;
+        g.B = p->W1; g.ldb = F; g.C = w.dv + t0 * D; g.ldc = D;
         g.M = r; g.N = D; g.K = F;
         RUN("gemm.bwd_dv", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
       }
-      if (G.dW1) {   // dW1 = v^T dZ
-        RUN("transpose.act", 0, tb * r * D, transpose(E, w.vg, D, 0, w.vgT, d.Rp, 0, r, D, rp, 1, s));
+      if (G.dW1) {   // dW1 = v^T dZ, v read token-major (dZ^T is zero past the group's rows)
         GemmArgs g;
-        g.A = w.vgT; g.lda = d.Rp; g.B = w.dzT; g.ldb = d.Rp; g.C = G.dW1; g.ldc = F;
+        g.A = w.vg; g.lda = D; g.trans_a = 1; g.a_rows = r;
+        g.B = w.dzT; g.ldb = d.Rp; g.C = G.dW1; g.ldc = F;
         g.M = D; g.N = F; g.K = rp; g.accumulate = first ? 0 : 1;
         RUN("gemm.bwd_dw1", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
       }
@@ -541,12 +534,15 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     g.A = w.dhe; g.lda = D; g.B = p->Wo; g.ldb = D; g.C = w.dO; g.ldc = D; g.M = T; g.N = D; g.K = D;
     RUN("gemm.bwd_do", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
   }
-  if (G.dWo) {
-    RUN("transpose.act", 0, tb * T * D, transpose(E, sv.o, D, S * D, w.oT, Tp, Sp, S, D, Sp, B, s));
+  if (G.dWo) {   // per sequence: O read token-major, dh from its zero-padded feature-major copy
     RUN("transpose.act", 0, tb * T * D, transpose(E, w.dhe, D, S * D, w.dhT, Tp, Sp, S, D, Sp, B, s));
-    GemmArgs g;
-    g.A = w.oT; g.lda = Tp; g.B = w.dhT; g.ldb = Tp; g.C = G.dWo; g.ldc = D; g.M = D; g.N = D; g.K = Tp;
-    RUN("gemm.bwd_dwo", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
+    for (int b = 0; b < B; ++b) {
+      GemmArgs g;
+      g.A = off(sv.o, b * S * D * E_); g.lda = D; g.trans_a = 1; g.a_rows = S;
+      g.B = off(w.dhT, b * Sp * E_); g.ldb = Tp; g.C = G.dWo; g.ldc = D;
+      g.M = D; g.N = D; g.K = Sp; g.accumulate = b > 0;
+      RUN("gemm.bwd_dwo", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
+    }
   }
 
   // ---- attention backward, probabilities rebuilt from the saved log-sum-exp
@@ -568,24 +564,26 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
   }
 
   // ---- QKV projection and LN1 backward
-  RUN("transpose.act", 0, tb * 3 * T * D, transpose(E, w.dqkvT, Tp, Sp, w.dqkv, 3 * D, S * 3 * D, 3 * D, S, 3 * D, B, s));
   if (G.dWq || G.dWk || G.dWv) {
     RUN("layernorm.fwd", 0, 2.0 * T * D * E_,
         layer_norm(E, E, X, D, p->ln1_g, p->ln1_b, w.u, D, sv.mu1, sv.rstd1, T, D, cfg->ln_eps, 1, s));
-    RUN("transpose.act", 0, tb * T * D, transpose(E, w.u, D, S * D, w.uT, Tp, Sp, S, D, Sp, B, s));
+    // per sequence: u read token-major; dQ^T, dK^T, dV^T are zero past the sequence end
     float* outs[3] = {G.dWq, G.dWk, G.dWv};
     for (int i = 0; i < 3; ++i) {
       if (!outs[i]) continue;
-      GemmArgs g;
-      g.A = w.uT; g.lda = Tp; g.B = off(w.dqkvT, i * D * Tp * E_); g.ldb = Tp; g.C = outs[i]; g.ldc = D;
-      g.M = D; g.N = D; g.K = Tp;
-      RUN("gemm.bwd_dwqkv", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
+      for (int b = 0; b < B; ++b) {
+        GemmArgs g;
+        g.A = off(w.u, b * S * D * E_); g.lda = D; g.trans_a = 1; g.a_rows = S;
+        g.B = off(w.dqkvT, (i * D * Tp + b * Sp) * E_); g.ldb = Tp; g.C = outs[i]; g.ldc = D;
+        g.M = D; g.N = D; g.K = Sp; g.accumulate = b > 0;
+        RUN("gemm.bwd_dwqkv", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
+      }
     }
   }
-  {
-    GemmArgs g;   // dU = [dQ dK dV] [Wq Wk Wv]^T
-    g.A = w.dqkv; g.lda = 3 * D; g.B = w.wcat; g.ldb = 3 * D; g.C = w.dU; g.ldc = D; g.M = T; g.N = D;
-    g.K = 3 * D;
+  for (int b = 0; b < B; ++b) {
+    GemmArgs g;   // dU = [dQ dK dV] [Wq Wk Wv]^T per sequence, [dQ dK dV] read feature-major
+    g.A = off(w.dqkvT, b * Sp * E_); g.lda = Tp; g.trans_a = 1; g.a_cols = Tp - b * Sp;
+    g.B = w.wcat; g.ldb = 3 * D; g.C = w.dU + b * S * D; g.ldc = D; g.M = S; g.N = D; g.K = 3 * D;
     RUN("gemm.bwd_du", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
   }
   RUN("layernorm.bwd", 0, (double)T * D * (E_ + 4 + 4 + EO),
