@@ -68,7 +68,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
   auto issue = [&](int it) {
     const int qt0 = qstart + 64 * (ntiles - 1 - it);
     char* st = smem + (it % C::NS) * C::STAGE;
-    ring_issue<DH, C::NW>(st, Qb, (int)a.ld_q, dOb, (int)a.ld_do, qt0, S - 1, wave, lane);
+    ring_issue<DH, C::NW>(st, Qb, (int)a.ld_q, qt0, dOb, (int)a.ld_do, qt0, S - 1, wave, lane);
     // base-2 lse and delta of the 64 queries (indices < Sp: in bounds; rows >= S are
     // masked); every wave copies them, so that all waves count the same copies
     dma4s(lse2 + qt0, 4u * lane, st + 2 * C::TB);
@@ -88,6 +88,9 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     // iff lo <= offset <= hi
     const int lo = a.causal ? key - qt0 : 0;
     const int hi = key < S ? S - 1 - qt0 : -1;
+    // the lane part of the offset moves into the bounds, so that every comparison is
+    // against a constant
+    const int lo4 = lo - 4 * (lane >> 5), hi4 = hi - 4 * (lane >> 5);
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
       // dP starts from -Delta of its query rows, so the MFMAs leave dP - Delta
@@ -113,7 +116,10 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * rg + e;
           float p = fast_exp2(fmaf(s[r], c, -l4[e]));
-          if constexpr (decltype(MASK)::value) p = (qi + e >= lo && qi + e <= hi) ? p : 0.0f;
+          if constexpr (decltype(MASK)::value) {
+            const int off = 32 * mt + 8 * rg + e;
+            p = (off >= lo4 && off <= hi4) ? p : 0.0f;
+          }
           s[r] = p;
           dp[r] = p * dp[r];                           // dS
         }

@@ -67,8 +67,8 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
   const RingOff<DH, C::NW> roff = ring_offsets<DH, C::NW>((int)a.ld_k, (int)a.ld_v, wave, lane);
   auto issue = [&](int j) {
     char* st = smem + (j % C::NS) * C::STAGE;
-    if (64 * j + 63 < S) ring_issue_full<DH, C::NW>(st, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, roff, wave);
-    else ring_issue<DH, C::NW>(st, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, S - 1, wave, lane);
+    if (64 * j + 63 < S) ring_issue_full<DH, C::NW>(st, Kb, (int)a.ld_k, 64 * j, Vb, (int)a.ld_v, 64 * j, roff, wave);
+    else ring_issue<DH, C::NW>(st, Kb, (int)a.ld_k, 64 * j, Vb, (int)a.ld_v, 64 * j, S - 1, wave, lane);
   };
 
   f32x16 acc[C::DT];                                // dQ^T of the wave's queries
@@ -89,11 +89,13 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
         s = mfma32x32x16(frag_rows<DH>(kt, 32 * mt, 2 * kk, lane), qf[kk], s);
         dp = mfma32x32x16(frag_rows<DH>(vt, 32 * mt, 2 * kk, lane), dof[kk], dp);
       }
-      const int lim = kv_last - kv0 - 32 * mt;
+      // key offset of register r: acc_row(r, lane); the lane part moves into the limit
+      // so that every comparison is against a constant
+      const int lim = kv_last - kv0 - 32 * mt - 4 * (lane >> 5);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float p = fast_exp2(fmaf(s[r], c, nlse2));
-        if constexpr (decltype(MASK)::value) p = (acc_row(r, lane) <= lim) ? p : 0.0f;
+        if constexpr (decltype(MASK)::value) p = (8 * (r >> 2) + (r & 3) <= lim) ? p : 0.0f;
         s[r] = p * dp[r];                           // dS^T
       }
 #pragma unroll

@@ -72,22 +72,24 @@ BPT_DEV int ring_block(int wave, int i) {
   return b < Ring2<DH, NW>::NB ? b : Ring2<DH, NW>::NB - 1;
 }
 
-// Issue this wave's copies of one stage. Rows past last_row are clamped to it (the
-// kernels mask them); row0 <= last_row.
+// Issue this wave's copies of one stage: rows row0 .. row0+63 of src0 into the first
+// tile, rows row1 .. row1+63 of src1 into the second. Rows past last_row are clamped
+// to it (the kernels mask them); row0, row1 <= last_row.
 template <int DH, int NW = 4>
-BPT_DEV void ring_issue(char* stage, const bf16* src0, int ld0, const bf16* src1, int ld1,
-                        int row0, int last_row, int wave, int lane) {
+BPT_DEV void ring_issue(char* stage, const bf16* src0, int ld0, int row0, const bf16* src1, int ld1, int row1,
+                        int last_row, int wave, int lane) {
   using T = RmTile<DH>;
   const bf16* org0 = src0 + (int64_t)row0 * ld0;
-  const bf16* org1 = src1 + (int64_t)row0 * ld1;
-  const int lim = last_row - row0 < 63 ? last_row - row0 : 63;
+  const bf16* org1 = src1 + (int64_t)row1 * ld1;
+  const int lim0 = last_row - row0 < 63 ? last_row - row0 : 63;
+  const int lim1 = last_row - row1 < 63 ? last_row - row1 : 63;
   // recomputed at every call: hoisting the offsets out of the tile loop would cost
   // one register each for the whole kernel
   asm volatile("" : "+v"(lane));
 #pragma unroll
   for (int i = 0; i < Ring2<DH, NW>::DPW; ++i) {
     const int b = ring_block<DH, NW>(wave, i), t = b >= T::BLOCKS, blk = b - t * T::BLOCKS;
-    const int slot = blk * 64 + lane, col = slot % T::SLOTS;
+    const int slot = blk * 64 + lane, col = slot % T::SLOTS, lim = t ? lim1 : lim0;
     int row = slot / T::SLOTS;
     row = row < lim ? row : lim;
     const uint32_t off = 2u * (uint32_t)(row * (t ? ld1 : ld0) + (col < DH / 8 ? col : 0) * 8);
@@ -116,13 +118,13 @@ BPT_DEV RingOff<DH, NW> ring_offsets(int ld0, int ld1, int wave, int lane) {
   return r;
 }
 
-// ring_issue for a full stage with precomputed offsets.
+// ring_issue for a stage whose rows all exist, with precomputed offsets.
 template <int DH, int NW>
-BPT_DEV void ring_issue_full(char* stage, const bf16* src0, int ld0, const bf16* src1, int ld1, int row0,
+BPT_DEV void ring_issue_full(char* stage, const bf16* src0, int ld0, int row0, const bf16* src1, int ld1, int row1,
                              const RingOff<DH, NW>& r, int wave) {
   using T = RmTile<DH>;
   const bf16* org0 = src0 + (int64_t)row0 * ld0;
-  const bf16* org1 = src1 + (int64_t)row0 * ld1;
+  const bf16* org1 = src1 + (int64_t)row1 * ld1;
 #pragma unroll
   for (int i = 0; i < Ring2<DH, NW>::DPW; ++i) {
     const int b = ring_block<DH, NW>(wave, i), t = b >= T::BLOCKS, blk = b - t * T::BLOCKS;

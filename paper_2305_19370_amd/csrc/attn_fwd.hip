@@ -82,8 +82,8 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
   const RingOff<DH, C::NW> roff = ring_offsets<DH, C::NW>((int)a.ld_k, (int)a.ld_v, wave, lane);
   auto issue = [&](int j) {
     char* st = smem + (j % C::NS) * C::STAGE;
-    if (64 * j + 63 < S) ring_issue_full<DH, C::NW>(st, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, roff, wave);
-    else ring_issue<DH, C::NW>(st, Kb, (int)a.ld_k, Vb, (int)a.ld_v, 64 * j, S - 1, wave, lane);
+    if (64 * j + 63 < S) ring_issue_full<DH, C::NW>(st, Kb, (int)a.ld_k, 64 * j, Vb, (int)a.ld_v, 64 * j, roff, wave);
+    else ring_issue<DH, C::NW>(st, Kb, (int)a.ld_k, 64 * j, Vb, (int)a.ld_v, 64 * j, S - 1, wave, lane);
   };
 
   f32x16 acc[C::DT];                                // O^T of the wave's queries
@@ -102,11 +102,13 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) s[mt] = mfma32x32x16(frag_rows<DH>(kt, 32 * mt, 2 * kk, lane), qf[kk], s[mt]);
     if constexpr (decltype(MASK)::value) {
-      const int lim = kv_last - kv0;
+      // key offset of register r: 32 mt + acc_row(r, lane); the lane part moves into the
+      // limit so that every comparison is against a constant
+      const int lim = kv_last - kv0 - 4 * (lane >> 5);
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s[mt][r] = (32 * mt + acc_row(r, lane) <= lim) ? s[mt][r] : NEG_INF;
+        for (int r = 0; r < 16; ++r) s[mt][r] = (32 * mt + 8 * (r >> 2) + (r & 3) <= lim) ? s[mt][r] : NEG_INF;
     }
     float mx = NEG_INF;
 #pragma unroll
