@@ -141,21 +141,22 @@ BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, float* c2, const 
 // touches over distinct bank groups. The copies apply the same permutation on the
 // global side, so a wave's 1 KiB copy block still lands contiguously. K must be a
 // multiple of 32 (host-checked).
-template <int BM, int BN>
+template <int BM, int BN, int NWN = 2>
 struct TileCfg {
   static constexpr int BK = 32;
   static constexpr int PITCH = 64;                     // bytes per tile row
-  static constexpr int WM = BM / 2, WN = BN / 2;      // wave tile (2 x 2 waves)
+  static constexpr int NW = 2 * NWN;                  // waves: 2 along M x NWN along N
+  static constexpr int WM = BM / 2, WN = BN / NWN;    // wave tile
   static constexpr int TM = WM / 32, TN = WN / 32;    // 32x32 MFMA tiles per wave
   static constexpr int ABYTES = BM * PITCH, BBYTES = BN * PITCH;
   static constexpr int ABLK = ABYTES / 1024, BBLK = BBYTES / 1024;    // 1 KB copy blocks
-  static constexpr int APW = (ABLK + 3) / 4, BPW = (BBLK + 3) / 4;    // copies per wave
+  static constexpr int APW = (ABLK + NW - 1) / NW, BPW = (BBLK + NW - 1) / NW;   // copies per wave
   static constexpr int DPS = APW + BPW;               // copy instructions per wave per stage
   static constexpr int STAGE = ABYTES + BBYTES;
   static constexpr int NS = 4;                        // stages in the ring
   static constexpr int LDS = NS * STAGE;
   static_assert(ABYTES % 1024 == 0 && BBYTES % 1024 == 0, "whole copy blocks");
-  static_assert(4 * (WN + 4) * 32 * 4 <= LDS, "epilogue staging fits");
+  static_assert(NW * (WN + 4) * 32 * 4 <= LDS, "epilogue staging fits");
 };
 
 // One wave copies 1 KiB from global memory straight into LDS: lane l's 16 bytes land at
@@ -207,13 +208,13 @@ BPT_DEV void tr_slot(int slot, int& row, int& col, int cols_left) {
   col = 8 * lc < cols_left - 8 ? 8 * lc : cols_left - 8;
 }
 
-template <int BM, int BN, int EPI, typename CT, typename RT, bool TA = false, bool TB = false>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
-  using Cfg = TileCfg<BM, BN>;
+template <int BM, int BN, int EPI, typename CT, typename RT, bool TA = false, bool TB = false, int NWN = 2>
+__global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
+  using Cfg = TileCfg<BM, BN, NWN>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / NWN, wn = wave % NWN;
   // Tile order. Workgroup i runs on XCD i % 8, and each XCD has its own L2. The ids are
   // renumbered so that every XCD owns a contiguous range of tiles; within the range,
   // tiles go down GM row blocks before moving to the next column block, so the ~32
@@ -247,7 +248,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
     const int alast = (int)(a.M - 1 - m0), blast = (int)(a.N - 1 - n0);
 #pragma unroll
     for (int i = 0; i < Cfg::APW; ++i) {
-      int blk = wave + 4 * i;
+      int blk = wave + Cfg::NW * i;
       blk = blk < Cfg::ABLK ? blk : Cfg::ABLK - 1;     // extra copies repeat the last block
       const int slot = blk * 64 + lane;
       if constexpr (TA) {
@@ -261,7 +262,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < Cfg::BPW; ++i) {
-      int blk = wave + 4 * i;
+      int blk = wave + Cfg::NW * i;
       blk = blk < Cfg::BBLK ? blk : Cfg::BBLK - 1;
       const int slot = blk * 64 + lane;
       if constexpr (TB) {
@@ -293,7 +294,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
     const uint32_t st = ring + (kt % Cfg::NS) * Cfg::STAGE;
     const int k0 = kt * Cfg::BK;
     if (d < Cfg::APW) {
-      int blk = wave + 4 * d;
+      int blk = wave + Cfg::NW * d;
       blk = blk < Cfg::ABLK ? blk : Cfg::ABLK - 1;
       if constexpr (TA)
         lds_dma16(tr_src(A, a.lda, arows, acols, k0, blk, aoff[d], std::integral_constant<int, BM>{}),
@@ -301,7 +302,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
       else
         lds_dma16(A + k0 + aoff[d], st + blk * 1024);
     } else {
-      int blk = wave + 4 * (d - Cfg::APW);
+      int blk = wave + Cfg::NW * (d - Cfg::APW);
       blk = blk < Cfg::BBLK ? blk : Cfg::BBLK - 1;
       if constexpr (TB)
         lds_dma16(tr_src(B, a.ldb, brows, bcols, k0, blk, boff[d - Cfg::APW], std::integral_constant<int, BN>{}),
@@ -523,10 +524,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 }
 
 // ------------------------------------------------------------------ dispatch
-template <int BM, int BN, int EPI, typename CT, typename RT, bool TA = false, bool TB = false>
+template <int BM, int BN, int EPI, typename CT, typename RT, bool TA = false, bool TB = false, int NWN = 2>
 static hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
-  using Cfg = TileCfg<BM, BN>;
-  auto kern = gemm_bf16_kernel<BM, BN, EPI, CT, RT, TA, TB>;
+  using Cfg = TileCfg<BM, BN, NWN>;
+  auto kern = gemm_bf16_kernel<BM, BN, EPI, CT, RT, TA, TB, NWN>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -538,9 +539,12 @@ static hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((ncols + BN - 1) / BN);
   if (tiles <= 0 || a.batch <= 0) return hipSuccess;
   if (a.K % Cfg::BK != 0) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(kern, dim3((unsigned)tiles, 1, (unsigned)a.batch), dim3(256), Cfg::LDS, s, a);
+  hipLaunchKernelGGL(kern, dim3((unsigned)tiles, 1, (unsigned)a.batch), dim3(64 * Cfg::NW), Cfg::LDS, s, a);
   return hipGetLastError();
 }
+
+// waves along N of the 256 x 256 tile configuration
+static constexpr int kNWN = 4;
 
 template <int EPI, typename CT, typename RT>
 static hipError_t launch_typed(Dt ab, const GemmArgs& a, hipStream_t s) {
@@ -560,18 +564,18 @@ static hipError_t launch_typed(Dt ab, const GemmArgs& a, hipStream_t s) {
           (a.trans_b && ((a.b_cols > 0 ? a.b_cols : a.N) % 8 || a.ldb % 8)))
         return hipErrorInvalidValue;
       if (a.trans_a && a.trans_b)
-        return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, true>(a, s)
+        return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, true, kNWN>(a, s)
                           : launch_bf16<128, 128, EPI, CT, RT, true, true>(a, s);
       if (a.trans_a)
-        return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, false>(a, s)
+        return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, false, kNWN>(a, s)
                           : launch_bf16<128, 128, EPI, CT, RT, true, false>(a, s);
-      return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, false, true>(a, s)
+      return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, false, true, kNWN>(a, s)
                         : launch_bf16<128, 128, EPI, CT, RT, false, true>(a, s);
     } else {
       return hipErrorInvalidValue;
     }
   }
-  if (big >= 256) return launch_bf16<256, 256, EPI, CT, RT>(a, s);
+  if (big >= 256) return launch_bf16<256, 256, EPI, CT, RT, false, false, kNWN>(a, s);
   return launch_bf16<128, 128, EPI, CT, RT>(a, s);
 }
 
