@@ -558,22 +558,26 @@ static hipError_t launch_typed(Dt ab, const GemmArgs& a, hipStream_t s) {
   }
   const int64_t big = ((a.M + 255) / 256) * ((ncols + 255) / 256) * a.batch;
   if (a.trans_a || a.trans_b) {
-    if constexpr (EPI == EPI_STORE) {
-      // a transposed operand is read in 16-byte column chunks
-      if ((a.trans_a && ((a.a_cols > 0 ? a.a_cols : a.M) % 8 || a.lda % 8)) ||
-          (a.trans_b && ((a.b_cols > 0 ? a.b_cols : a.N) % 8 || a.ldb % 8)))
-        return hipErrorInvalidValue;
-      if (a.trans_a && a.trans_b)
+    // a transposed operand is read in 16-byte column chunks
+    if ((a.trans_a && ((a.a_cols > 0 ? a.a_cols : a.M) % 8 || a.lda % 8)) ||
+        (a.trans_b && ((a.b_cols > 0 ? a.b_cols : a.N) % 8 || a.ldb % 8)))
+      return hipErrorInvalidValue;
+    // instantiated combinations: B transposed with every epilogue, A transposed with
+    // the plain store and the GELU epilogue, both with the plain store
+    if (a.trans_a && a.trans_b) {
+      if constexpr (EPI == EPI_STORE)
         return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, true, kNWN>(a, s)
                           : launch_bf16<128, 128, EPI, CT, RT, true, true>(a, s);
-      if (a.trans_a)
-        return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, false, kNWN>(a, s)
-                          : launch_bf16<128, 128, EPI, CT, RT, true, false>(a, s);
-      return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, false, true, kNWN>(a, s)
-                        : launch_bf16<128, 128, EPI, CT, RT, false, true>(a, s);
-    } else {
       return hipErrorInvalidValue;
     }
+    if (a.trans_a) {
+      if constexpr (EPI == EPI_STORE || EPI == EPI_GELU)
+        return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, false, kNWN>(a, s)
+                          : launch_bf16<128, 128, EPI, CT, RT, true, false>(a, s);
+      return hipErrorInvalidValue;
+    }
+    return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, false, true, kNWN>(a, s)
+                      : launch_bf16<128, 128, EPI, CT, RT, false, true>(a, s);
   }
   if (big >= 256) return launch_bf16<256, 256, EPI, CT, RT, false, false, kNWN>(a, s);
   return launch_bf16<128, 128, EPI, CT, RT>(a, s);

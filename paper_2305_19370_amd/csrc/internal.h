@@ -32,7 +32,8 @@ struct GemmArgs {
   int batch = 1;
   int accumulate = 0;          // fp32 C only: C += acc
   int bias_on_m = 0;           // EPI_GELU: bias indexed by row instead of column
-  // Transposed operands (EPI_STORE only): trans_a means A is stored K-major, element
+  // Transposed operands (trans_b with any epilogue, trans_a with EPI_STORE or EPI_GELU,
+  // both with EPI_STORE): trans_a means A is stored K-major, element
   // (m, k) at A[k * lda + m]; likewise trans_b for B (element (n, k) at B[k * ldb + n]).
   // For such an operand, x_rows is the number of k rows that may be read (rows from
   // x_rows up to K are not read, and the other operand must be zero at those k), and

@@ -119,16 +119,12 @@ SavedPtrs saved_layout(const Dims& d, void* base, int64_t* total) {
 }
 
 struct FwdWs {
-  void *wqkvT, *woT, *w1T, *w2T, *u, *vg, *gg;
+  void *u, *vg, *gg;
 };
 
 FwdWs fwd_ws(const Dims& d, void* base, int64_t* total) {
   Bump bp(base);
   FwdWs w;
-  w.wqkvT = bp.take(3 * d.D * d.D * d.E);
-  w.woT = bp.take(d.D * d.D * d.E);
-  w.w1T = bp.take(d.F * d.D * d.E);
-  w.w2T = bp.take(d.D * d.F * d.E);
   w.u = bp.take(d.T * d.D * d.E);
   w.vg = bp.take(d.R * d.D * d.E);
   w.gg = bp.take(d.R * d.F * d.E);
@@ -137,7 +133,7 @@ FwdWs fwd_ws(const Dims& d, void* base, int64_t* total) {
 }
 
 struct BwdWs {
-  void *w1T, *wcat;
+  void *wcat;
   void *vg, *gT, *dzT;
   float* gpT;
   float *dv, *dh, *dU, *delta, *lse2, *partial, *scratch;
@@ -147,7 +143,6 @@ struct BwdWs {
 BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
   Bump bp(base);
   BwdWs w;
-  w.w1T = bp.take(d.F * d.D * d.E);
   w.wcat = bp.take(3 * d.D * d.D * d.E);
   w.vg = bp.take(d.R * d.D * d.E);
   w.gT = bp.take(d.F * d.Rp * d.E);
@@ -377,22 +372,15 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
   const int64_t D = d.D, F = d.F, T = d.T, E_ = (int64_t)d.E;
   const size_t EO = esize(cfg->out_dtype);
 
-  // weights into the K-contiguous layouts the NT GEMMs read
-  const double wb = 2.0 * E_;
-  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wq, D, 0, w.wqkvT, D, 0, D, D, D, 1, s));
-  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wk, D, 0, off(w.wqkvT, D * D * E_), D, 0, D, D, D, 1, s));
-  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wv, D, 0, off(w.wqkvT, 2 * D * D * E_), D, 0, D, D, D, 1, s));
-  RUN("transpose.weights", 0, wb * D * D, transpose(E, p->Wo, D, 0, w.woT, D, 0, D, D, D, 1, s));
-  RUN("transpose.weights", 0, wb * D * F, transpose(E, p->W1, F, 0, w.w1T, D, 0, D, F, D, 1, s));
-  RUN("transpose.weights", 0, wb * D * F, transpose(E, p->W2, D, 0, w.w2T, F, 0, F, D, F, 1, s));
-
   // U = LN1(X); [Q | K | V] = U [Wq | Wk | Wv]  (Algorithm 1: project the input)
   RUN("layernorm.fwd", 0, 2.0 * T * D * E_,
       layer_norm(E, E, X, D, p->ln1_g, p->ln1_b, w.u, D, sv.mu1, sv.rstd1, T, D, cfg->ln_eps, 0, s));
-  {
+  // the weights [D_in, D_out] are read as they are: B operands stored K-major
+  const void* wqkv[3] = {p->Wq, p->Wk, p->Wv};
+  for (int i = 0; i < 3; ++i) {
     GemmArgs g;
-    g.A = w.u; g.lda = D; g.B = w.wqkvT; g.ldb = D; g.C = sv.qkv; g.ldc = 3 * D;
-    g.M = T; g.N = 3 * D; g.K = D;
+    g.A = w.u; g.lda = D; g.B = wqkv[i]; g.ldb = D; g.trans_b = 1;
+    g.C = off(sv.qkv, i * D * E_); g.ldc = 3 * D; g.M = T; g.N = D; g.K = D;
     RUN("gemm.qkv", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
   }
 
@@ -414,7 +402,7 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
       RUN("attn.fwd", 4.0 * d.dh * pairs, (3.0 * r + 2.0 * (s0 + r)) * D * E_, attn_fwd(E, a, s));
 
       GemmArgs go;     // h = X + O Wo
-      go.A = off(sv.o, t0 * D * E_); go.lda = D; go.B = w.woT; go.ldb = D;
+      go.A = off(sv.o, t0 * D * E_); go.lda = D; go.B = p->Wo; go.ldb = D; go.trans_b = 1;
       go.C = sv.h + t0 * D; go.ldc = D; go.R = off(X, t0 * D * E_); go.ldr = D;
       go.M = r; go.N = D; go.K = D;
       RUN("gemm.wo", gemm_flops(go), gemm_bytes(go, E_, 4) + (double)r * D * E_,
@@ -425,12 +413,12 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
                      D, cfg->ln_eps, 0, s));
 
       GemmArgs g1;     // G = GELU(LN2(h) W1 + b1)
-      g1.A = w.vg; g1.lda = D; g1.B = w.w1T; g1.ldb = D; g1.C = w.gg; g1.ldc = F;
+      g1.A = w.vg; g1.lda = D; g1.B = p->W1; g1.ldb = F; g1.trans_b = 1; g1.C = w.gg; g1.ldc = F;
       g1.bias = p->b1; g1.M = r; g1.N = F; g1.K = D;
       RUN("gemm.ffn1", gemm_flops(g1), gemm_bytes(g1, E_, E_), gemm(E, EPI_GELU, E, F32, g1, s));
 
       GemmArgs g2;     // Y = h + G W2 + b2
-      g2.A = w.gg; g2.lda = F; g2.B = w.w2T; g2.ldb = F; g2.C = off(Y, t0 * D * EO);
+      g2.A = w.gg; g2.lda = F; g2.B = p->W2; g2.ldb = D; g2.trans_b = 1; g2.C = off(Y, t0 * D * EO);
       g2.ldc = D; g2.R = sv.h + t0 * D; g2.ldr = D; g2.bias = p->b2; g2.M = r; g2.N = D; g2.K = F;
       RUN("gemm.ffn2", gemm_flops(g2), gemm_bytes(g2, E_, EO) + 4.0 * r * D, gemm(E, EPI_RESID, OUT, F32, g2, s));
     }
@@ -469,7 +457,6 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
   const int B = (int)d.B;
   const double tb = 2.0 * E_;   // bytes per element of a transpose / copy (read + write)
 
-  RUN("transpose.weights", 0, tb * D * F, transpose(E, p->W1, F, 0, w.w1T, D, 0, D, F, D, 1, s));
   RUN("copy.weights", 0, tb * D * D, copy2d(E, p->Wq, D, w.wcat, 3 * D, D, D, s));
   RUN("copy.weights", 0, tb * D * D, copy2d(E, p->Wk, D, off(w.wcat, D * E_), 3 * D, D, D, s));
   RUN("copy.weights", 0, tb * D * D, copy2d(E, p->Wv, D, off(w.wcat, 2 * D * E_), 3 * D, D, D, s));
@@ -485,7 +472,8 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
                      cfg->ln_eps, 1, s));
       {   // Z^T = W1^T v^T: G^T = GELU(Z^T + b1), GELU'(Z^T)
         GemmArgs g;
-        g.A = w.w1T; g.lda = D; g.B = w.vg; g.ldb = D; g.C = w.gT; g.ldc = d.Rp; g.C2 = w.gpT; g.ldc2 = d.Rp;
+        g.A = p->W1; g.lda = F; g.trans_a = 1; g.B = w.vg; g.ldb = D;
+        g.C = w.gT; g.ldc = d.Rp; g.C2 = w.gpT; g.ldc2 = d.Rp;
         g.bias = p->b1; g.bias_on_m = 1; g.M = F; g.N = r; g.Nstore = rp; g.K = D;
         RUN("gemm.bwd_ffn1_recompute", gemm_flops(g), gemm_bytes(g, E_, E_ + 4), gemm(E, EPI_GELU, E, F32, g, s));
       }
