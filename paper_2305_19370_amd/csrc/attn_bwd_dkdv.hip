@@ -19,7 +19,7 @@ struct DkvCfg {
   static constexpr int NW = 8;                      // waves per workgroup
   static constexpr int KEYS = 32 * NW;              // keys per workgroup
   static constexpr int TB = RmTile<DH>::BYTES;
-  static constexpr int STAGE = 2 * TB + 2 * 64 * 4; // Q, dO tiles; lse (base 2), delta
+  static constexpr int STAGE = 2 * TB + 2 * 64 * 4; // Q, dO tiles; lse (base 2), -Delta
   static constexpr int NS = 4;                      // stages in the ring
   static constexpr int LDS = NS * STAGE;
   static constexpr int DPS = Ring2<DH, NW>::DPW + 2;  // copies per wave per stage
@@ -47,7 +47,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
   const bf16* Vb = (const bf16*)a.v + (int64_t)b * a.S * a.ld_v + h * DH;
   const bf16* dOb = (const bf16*)a.dout + (int64_t)b * a.S * a.ld_do + h * DH;
   const float* lse2 = a.lse2 + ((int64_t)b * a.H + h) * a.Sp;
-  const float* delta = a.delta + ((int64_t)b * a.H + h) * a.Sp;
+  const float* ndelta = a.ndelta + ((int64_t)b * a.H + h) * a.Sp;
 
   bf16x8 kf[C::KSTEPS], vf[C::KSTEPS];
   {
@@ -69,10 +69,10 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     const int qt0 = qstart + 64 * (ntiles - 1 - it);
     char* st = smem + (it % C::NS) * C::STAGE;
     ring_issue<DH, C::NW>(st, Qb, (int)a.ld_q, qt0, dOb, (int)a.ld_do, qt0, S - 1, wave, lane);
-    // base-2 lse and delta of the 64 queries (indices < Sp: in bounds; rows >= S are
+    // base-2 lse and -Delta of the 64 queries (indices < Sp: in bounds; rows >= S are
     // masked); every wave copies them, so that all waves count the same copies
     dma4s(lse2 + qt0, 4u * lane, st + 2 * C::TB);
-    dma4s(delta + qt0, 4u * lane, st + 2 * C::TB + 256);
+    dma4s(ndelta + qt0, 4u * lane, st + 2 * C::TB + 256);
   };
 
   f32x16 adv[C::DT], adk[C::DT];
@@ -99,7 +99,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
       for (int rg = 0; rg < 4; ++rg) {
         const f32x4 d4 = *(const f32x4*)(ls + 64 + 32 * mt + 8 * rg + 4 * (lane >> 5));
 #pragma unroll
-        for (int e = 0; e < 4; ++e) dp[4 * rg + e] = -d4[e];
+        for (int e = 0; e < 4; ++e) dp[4 * rg + e] = d4[e];    // -Delta as stored
       }
       f32x16 s = f32x16{};
 #pragma unroll
@@ -202,7 +202,7 @@ __global__ __launch_bounds__(64) void attn_bwd_dkdv_f32_kernel(AttnArgs a) {
   const float* Vp = (const float*)a.v + (int64_t)h * DH;
   const float* dOp = (const float*)a.dout + (int64_t)h * DH;
   const float* lse = a.lse + ((int64_t)b * a.H + h) * a.Sp;
-  const float* delta = a.delta + ((int64_t)b * a.H + h) * a.Sp;
+  const float* ndelta = a.ndelta + ((int64_t)b * a.H + h) * a.Sp;
   for (int d = 0; d < DH; ++d) {
     Kown[d * 65 + tid] = kv < S ? Kp[(b * S + kv) * a.ld_k + d] : 0.0f;
     Vown[d * 65 + tid] = kv < S ? Vp[(b * S + kv) * a.ld_v + d] : 0.0f;
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(64) void attn_bwd_dkdv_f32_kernel(AttnArgs a) {
     if (tid < 16) {
       const int64_t q = qt0 + tid;
       ls[tid] = q < S ? lse[q] : 0.0f;
-      dls[tid] = q < S ? delta[q] : 0.0f;
+      dls[tid] = q < S ? ndelta[q] : 0.0f;
     }
     __syncthreads();
     for (int i = 0; i < 16; ++i) {
@@ -235,7 +235,7 @@ __global__ __launch_bounds__(64) void attn_bwd_dkdv_f32_kernel(AttnArgs a) {
       }
       const bool ok = q < S && kv < S && !(a.causal && kv > q);
       const float p = ok ? __expf(sv * scale - ls[i]) : 0.0f;
-      const float ds = p * (dpv - dls[i]);
+      const float ds = p * (dpv + dls[i]);
 #pragma unroll
       for (int d = 0; d < DH; ++d) {
         dv[d] = fmaf(p, dOs[i * DH + d], dv[d]);

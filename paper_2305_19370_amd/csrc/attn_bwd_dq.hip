@@ -57,9 +57,9 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
   }
   const int64_t sidx = ((int64_t)b * a.H + h) * a.Sp + qr;
   const float nlse2 = qok ? -a.lse2[sidx] : 0.0f;
-  const float dl = qok ? a.delta[sidx] : 0.0f;
+  const float ndl = qok ? a.ndelta[sidx] : 0.0f;   // -Delta
   settle(nlse2);
-  settle(dl);
+  settle(ndl);
   const int kv_last = !qok ? -1 : (a.causal ? qrow : S - 1);   // last key this query may see
 
   const int kv_end = a.causal ? (q0 + C::QROWS < S ? q0 + C::QROWS : S) : S;
@@ -83,7 +83,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
     for (int mt = 0; mt < 2; ++mt) {
       f32x16 s = f32x16{}, dp;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dp[r] = -dl;     // the MFMAs leave dP^T - Delta
+      for (int r = 0; r < 16; ++r) dp[r] = ndl;     // the MFMAs leave dP^T - Delta
 #pragma unroll
       for (int kk = 0; kk < C::KSTEPS; ++kk) {
         s = mfma32x32x16(frag_rows<DH>(kt, 32 * mt, 2 * kk, lane), qf[kk], s);
@@ -164,7 +164,7 @@ __global__ __launch_bounds__(64) void attn_bwd_dq_f32_kernel(AttnArgs a) {
   const float* dOp = (const float*)a.dout + (int64_t)h * DH;
   const int64_t sidx = ((int64_t)b * a.H + h) * a.Sp + q;
   const float lq = q < S ? a.lse[sidx] : 0.0f;
-  const float dl = q < S ? a.delta[sidx] : 0.0f;
+  const float ndl = q < S ? a.ndelta[sidx] : 0.0f;
   for (int d = 0; d < DH; ++d) {
     Qown[d * 65 + tid] = q < S ? Qp[(b * S + q) * a.ld_q + d] : 0.0f;
     dOown[d * 65 + tid] = q < S ? dOp[(b * S + q) * a.ld_do + d] : 0.0f;
@@ -192,7 +192,7 @@ __global__ __launch_bounds__(64) void attn_bwd_dq_f32_kernel(AttnArgs a) {
       }
       const bool ok = q < S && kv < S && !(a.causal && kv > q);
       const float p = ok ? __expf(sv * scale - lq) : 0.0f;
-      const float ds = p * (dpv - dl);
+      const float ds = p * (dpv + ndl);
 #pragma unroll
       for (int d = 0; d < DH; ++d) dq[d] = fmaf(ds, Ks[jj * DH + d], dq[d]);
     }

@@ -57,7 +57,7 @@ struct AttnArgs {
   // feature-major outputs: element (b, s, f) at row f, column b*Sp + s
   void* dqt = nullptr; void* dkt = nullptr; void* dvt = nullptr; int64_t ld_dt = 0;
   float* lse = nullptr;        // [B, H, Sp] natural log
-  const float* delta = nullptr;// [B, H, Sp]
+  const float* ndelta = nullptr;// [B, H, Sp] -Delta, Delta = rowsum(dO * O)
   const float* lse2 = nullptr; // [B, H, Sp] log-sum-exp in base 2 (backward)
   int64_t S = 0, Sp = 0;
   int B = 0, H = 0, dh = 0;
@@ -106,9 +106,9 @@ hipError_t col_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols,
 hipError_t row_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols, float* out,
                    int accumulate, hipStream_t s);
 
-// delta[b, h, s] = sum_d dO[b*S+s, h*dh+d] * O[b*S+s, h*dh+d]; lse2 = lse * log2(e);
+// ndelta[b, h, s] = -sum_d dO[b*S+s, h*dh+d] * O[b*S+s, h*dh+d]; lse2 = lse * log2(e);
 // both are 0 for the padding positions s >= S
-hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, const float* lse, float* delta,
+hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, const float* lse, float* ndelta,
                       float* lse2, int B, int64_t S, int64_t Sp, int H, int dh, hipStream_t s);
 
 }  // namespace bpt

@@ -136,7 +136,7 @@ struct BwdWs {
   void *wcat;
   void *vg, *gT, *dzT;
   float* gpT;
-  float *dv, *dh, *dU, *delta, *lse2, *partial, *scratch;
+  float *dv, *dh, *dU, *ndelta, *lse2, *partial, *scratch;
   void *dhe, *dhT, *dO, *dqkvT, *u;
 };
 
@@ -153,7 +153,7 @@ BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
   w.dhe = bp.take(d.T * d.D * d.E);
   w.dhT = bp.take(d.D * d.Tp * d.E);
   w.dO = bp.take(d.T * d.D * d.E);
-  w.delta = (float*)bp.take(d.B * d.H * d.Sp * 4);
+  w.ndelta = (float*)bp.take(d.B * d.H * d.Sp * 4);
   w.lse2 = (float*)bp.take(d.B * d.H * d.Sp * 4);
   w.dqkvT = bp.take(3 * d.D * d.Tp * d.E);
   w.u = bp.take(d.T * d.D * d.E);
@@ -534,7 +534,7 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
   }
 
   // ---- attention backward, probabilities rebuilt from the saved log-sum-exp
-  RUN("attn.delta", 0, 2.0 * T * D * E_, attn_delta(E, w.dO, sv.o, D, sv.lse, w.delta, w.lse2, B, S, Sp, (int)d.H, (int)d.dh, s));
+  RUN("attn.delta", 0, 2.0 * T * D * E_, attn_delta(E, w.dO, sv.o, D, sv.lse, w.ndelta, w.lse2, B, S, Sp, (int)d.H, (int)d.dh, s));
   {
     AttnArgs a;
     a.q = sv.qkv; a.ld_q = 3 * D;
@@ -542,7 +542,7 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     a.v = off(sv.qkv, 2 * D * E_); a.ld_v = 3 * D;
     a.dout = w.dO; a.ld_do = D;
     a.dqt = w.dqkvT; a.dkt = off(w.dqkvT, D * Tp * E_); a.dvt = off(w.dqkvT, 2 * D * Tp * E_); a.ld_dt = Tp;
-    a.lse = sv.lse; a.delta = w.delta; a.lse2 = w.lse2;
+    a.lse = sv.lse; a.ndelta = w.ndelta; a.lse2 = w.lse2;
     a.S = S; a.Sp = Sp; a.B = B; a.H = (int)d.H; a.dh = (int)d.dh; a.causal = cfg->causal;
     const double pairs = attn_pairs(0, S, S, cfg->causal) * d.H * B;
     // key-outer: S = Q K^T, dP = dO V^T, dV += P^T dO, dK += dS^T Q (4 contractions)
