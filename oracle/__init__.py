@@ -22,6 +22,11 @@ Contents
                for every output row it returns, and for every gradient when
                the upstream gradient is zero outside those rows. Used for
                sampled-output parity at full workload sizes.
+``bf16_model`` The plain definition with every matrix-multiply operand rounded
+               to bfloat16: how far any bf16-operand implementation lands
+               from the exact result on a given input (tolerance floor).
+``bf16_rows``  ``bf16_model`` restricted to selected query rows, like ``rows``
+               (the tolerance floor at full workload sizes).
 
 Every function is pinned by ``tests/test_oracle_*.py`` against brute-force
 loops, closed forms, invariants, finite differences and an independent

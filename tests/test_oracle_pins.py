@@ -421,3 +421,39 @@ def test_bf16_model_without_rounding_is_the_oracle(causal):
     mr = bf16_layer_fwd_bwd(X, p, H, causal, dY, EPS)     # rounding on: close, not equal
     rel = np.abs(mr["Y"] - Y).max() / np.abs(Y).max()
     assert 1e-5 < rel < 5e-2
+
+
+# ----------------------------------------------------------------------------- bf16 rounding model on rows
+@pytest.mark.parametrize("causal", [False, True])
+def test_bf16_rows_model_matches_full_model(causal):
+    """With dY zero outside the selected rows, the rows-restricted rounding model returns the
+    full rounding model's Y rows and every gradient (rounding included)."""
+    from oracle.bf16_model import bf16_layer_fwd_bwd, to_bf16
+    from oracle.bf16_rows import bf16_rows_fwd_bwd
+    rng = np.random.default_rng(17)
+    B, S, D, H, F = 2, 37, 16, 2, 32
+    p = rand_params(rng, D, F)
+    X, dY = rng.normal(size=(B, S, D)), to_bf16(rng.normal(size=(B, S, D)))
+    rows = np.array([0, 5, 18, 19, 36])
+    dYm = np.zeros_like(dY)
+    dYm[:, rows] = dY[:, rows]
+    full = bf16_layer_fwd_bwd(X, p, H, causal, dYm, EPS)
+    part = bf16_rows_fwd_bwd(X, p, H, causal, rows, dY[:, rows], EPS)
+    np.testing.assert_allclose(part["Y"], full["Y"][:, rows], rtol=0, atol=1e-12)
+    for k in list(GRAD_OF) + ["db1", "db2", "dln1_g", "dln1_b", "dln2_g", "dln2_b"]:
+        np.testing.assert_allclose(part[k], full[k], rtol=0, atol=1e-11, err_msg=k)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_bf16_rows_model_without_rounding_is_the_rows_oracle(causal):
+    from oracle.bf16_rows import bf16_rows_fwd_bwd
+    rng = np.random.default_rng(18)
+    B, S, D, H, F = 1, 29, 16, 2, 32
+    p = rand_params(rng, D, F)
+    X, dY = rng.normal(size=(B, S, D)), rng.normal(size=(B, S, D))
+    rows = np.array([2, 11, 28])
+    Yr, gr = oracle.rows_layer_fwd_bwd(X, p, H, causal, rows, dY[:, rows], EPS)
+    m = bf16_rows_fwd_bwd(X, p, H, causal, rows, dY[:, rows], EPS, round_operands=False)
+    np.testing.assert_allclose(m["Y"], Yr, rtol=0, atol=1e-12)
+    for k in GRAD_OF:
+        np.testing.assert_allclose(m[k], gr[k], rtol=0, atol=1e-11, err_msg=k)
