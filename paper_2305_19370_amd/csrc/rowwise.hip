@@ -28,8 +28,90 @@ template <> struct Vec4<bf16> {
   }
 };
 
+// 8 consecutive elements <-> 8 floats, with 16-byte accesses
+template <typename T> struct Vec8;
+template <> struct Vec8<float> {
+  static BPT_DEV void load(const float* p, float v[8]) {
+    const f32x4 a = *(const f32x4*)p, b = *(const f32x4*)(p + 4);
+    v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3]; v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
+  }
+  static BPT_DEV void store(float* p, const float v[8]) {
+    *(f32x4*)p = f32x4{v[0], v[1], v[2], v[3]};
+    *(f32x4*)(p + 4) = f32x4{v[4], v[5], v[6], v[7]};
+  }
+};
+template <> struct Vec8<bf16> {
+  static BPT_DEV void load(const bf16* p, float v[8]) {
+    const bf16x8 x = *(const bf16x8*)p;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (float)x[e];
+  }
+  static BPT_DEV void store(bf16* p, const float v[8]) {
+    bf16x8 x;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = (bf16)v[e];
+    *(bf16x8*)p = x;
+  }
+};
+
 // ------------------------------------------------------------------ LayerNorm forward
-// One wave per row; each lane walks groups of 4 columns. Two-pass mean / variance.
+// Rows of D = 512 NC: one wave per row holds the whole row in registers (NC chunks of 8
+// consecutive elements per lane, chunk c of lane l at columns 8 (l + 64 c)), so every
+// element is read once and written once. Two-pass mean / variance over the registers.
+template <typename TI, typename TO, int NC>
+__global__ __launch_bounds__(256) void ln_fwd_reg_kernel(const TI* x, int64_t ldx, const float* g,
+                                                         const float* bb, TO* out, int64_t ldo, float* mu,
+                                                         float* rstd, int64_t rows, float eps, int use_stats) {
+  constexpr int D = 512 * NC;
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const TI* xr = x + row * ldx;
+  float v[NC][8];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) Vec8<TI>::load(xr + 8 * (lane + 64 * c), v[c]);
+  float mean, rs;
+  if (!use_stats) {
+    float sm = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sm += v[c][e];
+    mean = warp_sum(sm) / (float)D;
+    float q = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) q = fmaf(v[c][e] - mean, v[c][e] - mean, q);
+    rs = 1.0f / sqrtf(warp_sum(q) / (float)D + eps);
+    if (lane == 0) {
+      mu[row] = mean;
+      rstd[row] = rs;
+    }
+  } else {
+    mean = mu[row];
+    rs = rstd[row];
+  }
+  TO* orow = out + row * ldo;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int d = 8 * (lane + 64 * c);
+    float gv[8], bv[8];
+    if (g) Vec8<float>::load(g + d, gv);
+    if (bb) Vec8<float>::load(bb + d, bv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float y = (v[c][e] - mean) * rs;
+      if (g) y *= gv[e];
+      if (bb) y += bv[e];
+      v[c][e] = y;
+    }
+    Vec8<TO>::store(orow + d, v[c]);
+  }
+}
+
+// Any D (a multiple of 4): one wave per row; each lane walks groups of 4 columns and
+// re-reads the row (from cache) for the variance and the output. Two-pass mean / variance.
 template <typename TI, typename TO>
 __global__ __launch_bounds__(256) void ln_fwd_kernel(const TI* x, int64_t ldx, const float* g,
                                                      const float* bb, TO* out, int64_t ldo, float* mu,
@@ -82,6 +164,51 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const TI* x, int64_t ldx, c
 
 // ------------------------------------------------------------------ LayerNorm backward
 // dz = rstd * (gd - mean(gd) - xhat * mean(gd * xhat)), gd = dout * gamma; out = resid + dz.
+// Rows of D = 512 NC, row of x and of dout held in registers as in ln_fwd_reg_kernel.
+template <typename TI, typename TR, typename TO, typename T2, int NC>
+__global__ __launch_bounds__(256) void ln_bwd_reg_kernel(const TI* x, const float* mu, const float* rstd,
+                                                         const float* g, const float* dout, const TR* resid,
+                                                         TO* out, T2* out2, int64_t rows) {
+  constexpr int D = 512 * NC;
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float m = mu[row], rs = rstd[row];
+  float xh[NC][8], gd[NC][8];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int d = 8 * (lane + 64 * c);
+    Vec8<TI>::load(x + row * D + d, xh[c]);
+    Vec8<float>::load(dout + row * D + d, gd[c]);
+  }
+  float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    float gv[8];
+    if (g) Vec8<float>::load(g + 8 * (lane + 64 * c), gv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (g) gd[c][e] *= gv[e];
+      xh[c][e] = (xh[c][e] - m) * rs;
+      s1 += gd[c][e];
+      s2 = fmaf(gd[c][e], xh[c][e], s2);
+    }
+  }
+  s1 = warp_sum(s1) / (float)D;
+  s2 = warp_sum(s2) / (float)D;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int d = 8 * (lane + 64 * c);
+    float rv[8];
+    Vec8<TR>::load(resid + row * D + d, rv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) rv[e] += rs * (gd[c][e] - s1 - xh[c][e] * s2);
+    Vec8<TO>::store(out + row * D + d, rv);
+    if (out2) Vec8<T2>::store(out2 + row * D + d, rv);
+  }
+}
+
+// Any D (a multiple of 4).
 template <typename TI, typename TR, typename TO, typename T2>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(const TI* x, const float* mu, const float* rstd,
                                                      const float* g, const float* dout, const TR* resid,
@@ -268,6 +395,22 @@ hipError_t layer_norm(Dt ti, Dt to, const void* x, int64_t ldx, const float* g, 
                       int use_stats, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   const dim3 grid((unsigned)((rows + 3) / 4));
+  // register-resident rows when D = 512 NC and every row starts 16-byte aligned
+  const bool vec = D % 512 == 0 && ldx % 8 == 0 && ldo % 8 == 0 && ((uintptr_t)x & 15) == 0 &&
+                   ((uintptr_t)out & 15) == 0 && ((uintptr_t)g & 15) == 0 && ((uintptr_t)b & 15) == 0;
+#define BPT_LN_FWD(NCV)                                                                                  \
+  BPT_T(ti, TI, BPT_T(to, TO,                                                                            \
+        hipLaunchKernelGGL((ln_fwd_reg_kernel<TI, TO, NCV>), grid, dim3(256), 0, s, (const TI*)x, ldx, g, \
+                           b, (TO*)out, ldo, mu, rstd, rows, eps, use_stats)))
+  switch (vec ? D / 512 : 0) {
+    case 1: BPT_LN_FWD(1); return hipGetLastError();
+    case 2: BPT_LN_FWD(2); return hipGetLastError();
+    case 4: BPT_LN_FWD(4); return hipGetLastError();
+    case 8: BPT_LN_FWD(8); return hipGetLastError();
+    case 10: BPT_LN_FWD(10); return hipGetLastError();
+    default: break;
+  }
+#undef BPT_LN_FWD
   BPT_T(ti, TI, BPT_T(to, TO,
         hipLaunchKernelGGL((ln_fwd_kernel<TI, TO>), grid, dim3(256), 0, s, (const TI*)x, ldx, g, b,
                            (TO*)out, ldo, mu, rstd, rows, D, eps, use_stats)));
@@ -279,6 +422,22 @@ hipError_t layer_norm_bwd(Dt ti, const void* x, const float* mu, const float* rs
                           void* out2, int64_t rows, int64_t D, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   const dim3 grid((unsigned)((rows + 3) / 4));
+  const bool vec = D % 512 == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)dout & 15) == 0 &&
+                   ((uintptr_t)resid & 15) == 0 && ((uintptr_t)out & 15) == 0 && ((uintptr_t)out2 & 15) == 0 &&
+                   ((uintptr_t)g & 15) == 0;
+#define BPT_LN_BWD(NCV)                                                                                  \
+  BPT_T(ti, TI, BPT_T(tr, TR, BPT_T(to, TO, BPT_T(t2, T2,                                               \
+        hipLaunchKernelGGL((ln_bwd_reg_kernel<TI, TR, TO, T2, NCV>), grid, dim3(256), 0, s, (const TI*)x, \
+                           mu, rstd, g, dout, (const TR*)resid, (TO*)out, (T2*)out2, rows)))))
+  switch (vec ? D / 512 : 0) {
+    case 1: BPT_LN_BWD(1); return hipGetLastError();
+    case 2: BPT_LN_BWD(2); return hipGetLastError();
+    case 4: BPT_LN_BWD(4); return hipGetLastError();
+    case 8: BPT_LN_BWD(8); return hipGetLastError();
+    case 10: BPT_LN_BWD(10); return hipGetLastError();
+    default: break;
+  }
+#undef BPT_LN_BWD
   BPT_T(ti, TI, BPT_T(tr, TR, BPT_T(to, TO, BPT_T(t2, T2,
         hipLaunchKernelGGL((ln_bwd_kernel<TI, TR, TO, T2>), grid, dim3(256), 0, s, (const TI*)x, mu,
                            rstd, g, dout, (const TR*)resid, (TO*)out, (T2*)out2, rows, D)))));
