@@ -522,7 +522,15 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     g.A = w.dhe; g.lda = D; g.B = p->Wo; g.ldb = D; g.C = w.dO; g.ldc = D; g.M = T; g.N = D; g.K = D;
     RUN("gemm.bwd_do", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
   }
-  if (G.dWo) {   // per sequence: O read token-major, dh from its zero-padded feature-major copy
+  if (G.dWo && S % 32 == 0) {   // per sequence: O and dh both read token-major (K = S exactly)
+    for (int b = 0; b < B; ++b) {
+      GemmArgs g;
+      g.A = off(sv.o, b * S * D * E_); g.lda = D; g.trans_a = 1;
+      g.B = off(w.dhe, b * S * D * E_); g.ldb = D; g.trans_b = 1; g.C = G.dWo; g.ldc = D;
+      g.M = D; g.N = D; g.K = S; g.accumulate = b > 0;
+      RUN("gemm.bwd_dwo", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
+    }
+  } else if (G.dWo) {   // O read token-major, dh from its zero-padded feature-major copy
     RUN("transpose.act", 0, tb * T * D, transpose(E, w.dhe, D, S * D, w.dhT, Tp, Sp, S, D, Sp, B, s));
     for (int b = 0; b < B; ++b) {
       GemmArgs g;
