@@ -298,10 +298,11 @@ size_t bpt_describe(const bpt_config* cfg, char* buf, size_t n) {
   int w = snprintf(buf, n,
                    "dtype=%s attention: q-tile=%d kv-step=%d (%s); backward dK/dV kv-tile=%d q-step=%d, "
                    "dQ q-tile=%d kv-step=%d; gemm: %s; ffn group rows=%lld (%lld query blocks of %lld)",
-                   bf ? "bf16" : "f32", bf ? 128 : 64, bf ? 64 : 32,
-                   bf ? "MFMA 32x32x16 bf16, fp32 accumulate" : "fp32 VALU",
-                   bf ? 128 : 64, bf ? 64 : 16, bf ? 128 : 64, bf ? 64 : 16,
-                   bf ? "MFMA bf16 256x256 or 128x128 tiles, K-step 64" : "fp32 VALU 64x64 tiles",
+                   bf ? "bf16" : "f32", bf ? 256 : 64, bf ? 64 : 32,
+                   bf ? "MFMA 32x32x16 bf16, fp32 accumulate, 32 rows per wave" : "fp32 VALU",
+                   bf ? 256 : 64, bf ? 64 : 16, bf ? 256 : 64, bf ? 64 : 16,
+                   bf ? "MFMA bf16 256x256 (8 waves) or 128x128 (4 waves) tiles, K-step 32"
+                      : "fp32 VALU 64x64 tiles",
                    (long long)d.R, (long long)((d.R + cfg->Bq - 1) / cfg->Bq), (long long)cfg->Bq);
   return w < 0 ? 0 : std::min((size_t)w, n - 1);
 }
