@@ -5,6 +5,8 @@
 #include <stdint.h>
 
 typedef __bf16 bf16;
+typedef _Float16 f16;
+typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
@@ -17,10 +19,12 @@ typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
 template <typename T> BPT_DEV float to_f32(T x);
 template <> BPT_DEV float to_f32<float>(float x) { return x; }
 template <> BPT_DEV float to_f32<bf16>(bf16 x) { return (float)x; }
+template <> BPT_DEV float to_f32<f16>(f16 x) { return (float)x; }
 
 template <typename T> BPT_DEV T from_f32(float x);
 template <> BPT_DEV float from_f32<float>(float x) { return x; }
 template <> BPT_DEV bf16 from_f32<bf16>(float x) { return (bf16)x; }   // round to nearest even
+template <> BPT_DEV f16 from_f32<f16>(float x) { return (f16)x; }      // round to nearest even
 
 // One bf16 MFMA step: 32x32 output tile, K = 16, fp32 accumulation.
 // Operand layout (lane l of a wave64): A row (l % 32), B column (l % 32), each lane

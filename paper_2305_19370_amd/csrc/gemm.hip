@@ -17,13 +17,27 @@
 
 namespace bpt {
 
+// GELU' output C2, element idx: fp32 or fp16 (a.c2t)
+BPT_DEV void c2_store(const GemmArgs& a, int64_t idx, float v) {
+  if (a.c2t == F16) ((f16*)a.C2)[idx] = (f16)v;
+  else ((float*)a.C2)[idx] = v;
+}
+BPT_DEV void c2_store4(const GemmArgs& a, int64_t idx, f32x4 v) {
+  if (a.c2t == F16) {
+    const f16x4 h = {(f16)v[0], (f16)v[1], (f16)v[2], (f16)v[3]};
+    *(f16x4*)((f16*)a.C2 + idx) = h;
+  } else {
+    *(f32x4*)((float*)a.C2 + idx) = v;
+  }
+}
+
 template <int EPI, typename CT, typename RT>
 BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float v) {
   CT* C = (CT*)a.C + z * a.sC;
   const int64_t idx = m * a.ldc + n;
   if (n >= a.N) {                                   // zero padding columns
     C[idx] = from_f32<CT>(0.0f);
-    if (EPI == EPI_GELU && a.C2) a.C2[z * a.sC2 + m * a.ldc2 + n] = 0.0f;
+    if (EPI == EPI_GELU && a.C2) c2_store(a, z * a.sC2 + m * a.ldc2 + n, 0.0f);
     return;
   }
   if constexpr (EPI == EPI_STORE) {
@@ -39,10 +53,10 @@ BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float
   } else if constexpr (EPI == EPI_GELU) {
     if (a.bias) v += a.bias[a.bias_on_m ? m : n];
     C[idx] = from_f32<CT>(gelu_f(v));
-    if (a.C2) a.C2[z * a.sC2 + m * a.ldc2 + n] = gelu_grad_f(v);
+    if (a.C2) c2_store(a, z * a.sC2 + m * a.ldc2 + n, gelu_grad_f(v));
   } else {  // EPI_MUL
-    const float* R = (const float*)a.R + z * a.sR;
-    C[idx] = from_f32<CT>(v * R[m * a.ldr + n]);
+    const RT* R = (const RT*)a.R + z * a.sR;
+    C[idx] = from_f32<CT>(v * to_f32<RT>(R[m * a.ldr + n]));
   }
 }
 
@@ -50,6 +64,12 @@ template <typename T> struct V4;
 template <> struct V4<float> {
   static BPT_DEV f32x4 ld(const float* p) { return *(const f32x4*)p; }
   static BPT_DEV void st(float* p, f32x4 v) { *(f32x4*)p = v; }
+};
+template <> struct V4<f16> {
+  static BPT_DEV f32x4 ld(const f16* p) {
+    const f16x4 x = *(const f16x4*)p;
+    return f32x4{(float)x[0], (float)x[1], (float)x[2], (float)x[3]};
+  }
 };
 template <> struct V4<bf16> {
   static BPT_DEV f32x4 ld(const bf16* p) {
@@ -94,18 +114,18 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
       v[e] = g;
       d[e] = gp;
     }
-    if (a.C2) *(f32x4*)(a.C2 + z * a.sC2 + m * a.ldc2 + n) = d;
+    if (a.C2) c2_store4(a, z * a.sC2 + m * a.ldc2 + n, d);
   } else {
-    v *= *(const f32x4*)((const float*)a.R + z * a.sR + m * a.ldr + n);
+    v *= V4<RT>::ld((const RT*)a.R + z * a.sR + m * a.ldr + n);
   }
   V4<CT>::st(C, v);
 }
 
 // Four consecutive columns n..n+3 of row m inside the stored width, from pointers
-// already at (m, n): c into C, r into R (EPI_RESID / EPI_MUL), c2 into C2 (EPI_GELU),
-// bn at bias[n]; bm = bias[m] for a per-row bias.
+// already at (m, n): c into C, r into R (EPI_RESID / EPI_MUL); c2 is the element index
+// of (m, n) in C2 (EPI_GELU); bn at bias[n]; bm = bias[m] for a per-row bias.
 template <int EPI, typename CT, typename RT>
-BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, float* c2, const float* bn, float bm, f32x4 v) {
+BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const float* bn, float bm, f32x4 v) {
   if constexpr (EPI == EPI_STORE) {
     if constexpr (sizeof(CT) == 4) {
       if (a.accumulate) v += V4<CT>::ld(c);
@@ -126,9 +146,9 @@ BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, float* c2, const 
       v[e] = g;
       d[e] = gp;
     }
-    if (a.C2) *(f32x4*)c2 = d;
+    if (a.C2) c2_store4(a, c2, d);
   } else {
-    v *= *(const f32x4*)r;
+    v *= V4<RT>::ld((const RT*)r);
   }
   V4<CT>::st(c, v);
 }
@@ -446,10 +466,10 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
       CT* cb = (CT*)a.C + z * a.sC + (mrow + r0) * a.ldc + ncol + c0;
       const char* rb = nullptr;
       if constexpr (EPI == EPI_RESID) rb = (const char*)((const RT*)a.R + z * a.sR + (mrow + r0) * a.ldr + ncol + c0);
-      else if constexpr (EPI == EPI_MUL) rb = (const char*)((const float*)a.R + z * a.sR + (mrow + r0) * a.ldr + ncol + c0);
-      float* c2b = (EPI == EPI_GELU && a.C2) ? a.C2 + z * a.sC2 + (mrow + r0) * a.ldc2 + ncol + c0 : nullptr;
+      else if constexpr (EPI == EPI_MUL) rb = (const char*)((const RT*)a.R + z * a.sR + (mrow + r0) * a.ldr + ncol + c0);
+      const int64_t c2b = z * a.sC2 + (mrow + r0) * a.ldc2 + ncol + c0;
       const float* bb = a.bias ? a.bias + ncol + c0 : nullptr;
-      constexpr int RS = EPI == EPI_MUL ? 4 : (int)sizeof(RT);
+      constexpr int RS = (int)sizeof(RT);
       constexpr int RSTEP = 64 / C4;                 // rows per iteration
       // the GELU epilogue is long: keep its loop rolled (instruction cache)
       constexpr int UNR = EPI == EPI_GELU ? 4 : 32 / RSTEP;
@@ -592,6 +612,9 @@ hipError_t gemm(Dt ab, Epi epi, Dt ct, Dt rt, const GemmArgs& a, hipStream_t s) 
       return ct == F32 ? launch_typed<EPI_GELU, float, float>(ab, a, s)
                        : launch_typed<EPI_GELU, bf16, float>(ab, a, s);
     case EPI_MUL:
+      if (rt == F16)
+        return ct == F32 ? launch_typed<EPI_MUL, float, f16>(ab, a, s)
+                         : launch_typed<EPI_MUL, bf16, f16>(ab, a, s);
       return ct == F32 ? launch_typed<EPI_MUL, float, float>(ab, a, s)
                        : launch_typed<EPI_MUL, bf16, float>(ab, a, s);
     case EPI_RESID:

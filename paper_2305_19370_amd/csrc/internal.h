@@ -6,7 +6,8 @@
 
 namespace bpt {
 
-enum Dt { F32 = 0, BF16 = 1 };
+// F16 is used for one tensor only: GELU'(z) saved by the FFN recompute of the bf16 path.
+enum Dt { F32 = 0, BF16 = 1, F16 = 2 };
 
 // ---------------------------------------------------------------- GEMM
 // C[M, N] = A[M, K] * B[N, K]^T ("NT": both operands K-contiguous), fp32 accumulation,
@@ -15,7 +16,7 @@ enum Epi {
   EPI_STORE = 0,   // C = acc            (fp32 C may accumulate: C += acc)
   EPI_RESID = 1,   // C = acc + R[m, n] (+ bias[n])
   EPI_GELU = 2,    // z = acc (+ bias[n] or bias[m]); C = GELU(z); C2 = GELU'(z) if C2
-  EPI_MUL = 3,     // C = acc * R[m, n]  (R fp32)
+  EPI_MUL = 3,     // C = acc * R[m, n]  (R fp32 or fp16)
 };
 
 struct GemmArgs {
@@ -24,7 +25,8 @@ struct GemmArgs {
   void* C = nullptr;
   const void* R = nullptr;     // residual (EPI_RESID) or multiplier (EPI_MUL)
   const float* bias = nullptr;
-  float* C2 = nullptr;         // second output of EPI_GELU
+  void* C2 = nullptr;          // second output of EPI_GELU, element type c2t (F32 or F16)
+  Dt c2t = F32;
   int64_t M = 0, N = 0, K = 0;
   int64_t Nstore = 0;          // columns [N, Nstore) of C (and C2) are written with 0
   int64_t lda = 0, ldb = 0, ldc = 0, ldr = 0, ldc2 = 0;

@@ -135,7 +135,7 @@ FwdWs fwd_ws(const Dims& d, void* base, int64_t* total) {
 struct BwdWs {
   void *wcat;
   void *vg, *gT, *dzT;
-  float* gpT;
+  void* gpT;             // GELU'(Z^T): fp32 on the fp32 path, fp16 on the bf16 path
   float *dv, *dh, *dU, *ndelta, *lse2, *partial, *scratch;
   void *dhe, *dhT, *dO, *dqkvT, *u;
 };
@@ -146,7 +146,7 @@ BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
   w.wcat = bp.take(3 * d.D * d.D * d.E);
   w.vg = bp.take(d.R * d.D * d.E);
   w.gT = bp.take(d.F * d.Rp * d.E);
-  w.gpT = (float*)bp.take(d.F * d.Rp * 4);
+  w.gpT = bp.take(d.F * d.Rp * (d.E == 2 ? 2 : 4));   // fp16 on the bf16 path, else fp32
   w.dzT = bp.take(d.F * d.Rp * d.E);
   w.dv = (float*)bp.take(d.T * d.D * 4);
   w.dh = (float*)bp.take(d.T * d.D * 4);
@@ -457,6 +457,10 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
   const size_t EO = esize(cfg->out_dtype);
   const int B = (int)d.B;
   const double tb = 2.0 * E_;   // bytes per element of a transpose / copy (read + write)
+  // GELU'(Z) between the FFN recompute and dZ: fp16 on the bf16 path (its rounding,
+  // 2^-11 relative, is far below the bf16 rounding of the dZ operand that follows)
+  const Dt GP = E == BF16 ? F16 : F32;
+  const int64_t GP_ = GP == F16 ? 2 : 4;
 
   RUN("copy.weights", 0, tb * D * D, copy2d(E, p->Wq, D, w.wcat, 3 * D, D, D, s));
   RUN("copy.weights", 0, tb * D * D, copy2d(E, p->Wk, D, off(w.wcat, D * E_), 3 * D, D, D, s));
@@ -474,15 +478,15 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
       {   // Z^T = W1^T v^T: G^T = GELU(Z^T + b1), GELU'(Z^T)
         GemmArgs g;
         g.A = p->W1; g.lda = F; g.trans_a = 1; g.B = w.vg; g.ldb = D;
-        g.C = w.gT; g.ldc = d.Rp; g.C2 = w.gpT; g.ldc2 = d.Rp;
+        g.C = w.gT; g.ldc = d.Rp; g.C2 = w.gpT; g.ldc2 = d.Rp; g.c2t = GP;
         g.bias = p->b1; g.bias_on_m = 1; g.M = F; g.N = r; g.Nstore = rp; g.K = D;
-        RUN("gemm.bwd_ffn1_recompute", gemm_flops(g), gemm_bytes(g, E_, E_ + 4), gemm(E, EPI_GELU, E, F32, g, s));
+        RUN("gemm.bwd_ffn1_recompute", gemm_flops(g), gemm_bytes(g, E_, E_ + GP_), gemm(E, EPI_GELU, E, F32, g, s));
       }
       {   // dZ^T = (W2 dY^T) * GELU'(Z^T)
         GemmArgs g;
         g.A = p->W2; g.lda = D; g.B = dYg; g.ldb = D; g.C = w.dzT; g.ldc = d.Rp; g.R = w.gpT; g.ldr = d.Rp;
         g.M = F; g.N = r; g.Nstore = rp; g.K = D;
-        RUN("gemm.bwd_dz", gemm_flops(g), gemm_bytes(g, E_, E_ + 4), gemm(E, EPI_MUL, E, F32, g, s));
+        RUN("gemm.bwd_dz", gemm_flops(g), gemm_bytes(g, E_, E_ + GP_), gemm(E, EPI_MUL, E, GP, g, s));
       }
       if (G.db1) RUN("reduce.bias", 0, (double)F * r * E_, row_sum(E, w.dzT, d.Rp, F, r, G.db1, first ? 0 : 1, s));
       if (G.dW2) {   // dW2 = G^T dY, dY read token-major (G^T is zero past the group's rows)
