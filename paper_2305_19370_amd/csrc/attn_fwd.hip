@@ -44,6 +44,9 @@ struct FwdCfg {
 // rescaled: exp-weights stay <= 2^8, and the final division uses the same
 // reference maximum, so the result is unchanged.
 static constexpr float RESCALE_LOG2 = 8.0f;
+// Largest per-lane sum of one tile's exp-weights (32 keys) accepted without computing
+// the tile's maximum.
+static constexpr float SUM_MAX = 65536.0f;
 
 template <int DH>
 __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
@@ -91,31 +94,9 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
   for (int t = 0; t < C::DT; ++t) acc[t] = f32x16{};
   float m_run = NEG_INF, l_run = 0.0f;
 
-  auto tile = [&](int j, auto MASK) {
-    const int kv0 = 64 * j;
-    const char* kt = smem + (j % C::NS) * C::STAGE;
-    const char* vt = kt + C::TB;
-    // S^T[key, query] = K Q^T
-    f32x16 s[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-    for (int kk = 0; kk < C::KSTEPS; ++kk)
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt) s[mt] = mfma32x32x16(frag_rows<DH>(kt, 32 * mt, 2 * kk, lane), qf[kk], s[mt]);
-    if constexpr (decltype(MASK)::value) {
-      // key offset of register r: 32 mt + acc_row(r, lane); the lane part moves into the
-      // limit so that every comparison is against a constant
-      const int lim = kv_last - kv0 - 4 * (lane >> 5);
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[mt][r] = (32 * mt + 8 * (r >> 2) + (r & 3) <= lim) ? s[mt][r] : NEG_INF;
-    }
-    float mx = NEG_INF;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
-    mx = max_halves(mx);
+  // Rescale the running numerator and sum to a new reference maximum mx (per lane);
+  // lanes whose maximum grew by at most RESCALE_LOG2 keep their reference.
+  auto rescale = [&](float mx) {
     const bool up = (mx - m_run) * c > RESCALE_LOG2;      // true on the first visible tile
     if (__ballot(up)) {
       asm volatile("" ::: "memory");                       // keep the rescale behind the branch
@@ -125,23 +106,81 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
       for (int t = 0; t < C::DT; ++t) acc[t] *= corr;
     }
     if (up) m_run = mx;
+  };
+  auto row_max = [&](const f32x16 (&s)[2]) {
+    float mx = NEG_INF;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
+    return max_halves(mx);
+  };
+  // exp-weights of the tile against the current reference maximum, and their sum
+  auto weights = [&](const f32x16 (&s)[2], f32x16 (&p)[2]) {
     const float mc = (m_run == NEG_INF ? 0.0f : m_run) * c;
     float rs = 0.0f;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(fmaf(s[mt][r], c, -mc));
-        s[mt][r] = p;
-        rs += p;
+        p[mt][r] = fast_exp2(fmaf(s[mt][r], c, -mc));
+        rs += p[mt][r];
       }
+    return rs;
+  };
+
+  // EXACT: the reference maximum follows the tile's row maximum (the first tile of
+  // every wave, which sets a finite reference on every row). Otherwise the weights are
+  // taken against the current reference first, and the maximum is only computed when
+  // a lane's sum of weights exceeds SUM_MAX (a score above the reference by more than
+  // about log2(SUM_MAX / 32) / c); every weight then stays <= SUM_MAX, and no row sum can
+  // vanish because the first tile left a weight of 1 at its maximum.
+  auto tile = [&](int j, auto MASK, auto EXACT) {
+    const int kv0 = 64 * j;
+    const char* kt = smem + (j % C::NS) * C::STAGE;
+    const char* vt = kt + C::TB;
+    // K fragments of the whole tile, read at once so that only the first MFMA waits
+    bf16x8 kf[C::KSTEPS][2];
+#pragma unroll
+    for (int kk = 0; kk < C::KSTEPS; ++kk)
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) kf[kk][mt] = frag_rows<DH>(kt, 32 * mt, 2 * kk, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    // S^T[key, query] = K Q^T
+    f32x16 s[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int kk = 0; kk < C::KSTEPS; ++kk)
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) s[mt] = mfma32x32x16(kf[kk][mt], qf[kk], s[mt]);
+    if constexpr (decltype(MASK)::value) {
+      // key offset of register r: 32 mt + acc_row(r, lane); the lane part moves into the
+      // limit so that every comparison is against a constant
+      const int lim = kv_last - kv0 - 4 * (lane >> 5);
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[mt][r] = (32 * mt + 8 * (r >> 2) + (r & 3) <= lim) ? s[mt][r] : NEG_INF;
+    }
+    f32x16 p[2];
+    float rs;
+    if constexpr (decltype(EXACT)::value) {
+      rescale(row_max(s));
+      rs = weights(s, p);
+    } else {
+      rs = weights(s, p);
+      if (__ballot(!(rs <= SUM_MAX))) {
+        asm volatile("" ::: "memory");
+        rescale(row_max(s));
+        rs = weights(s, p);
+      }
+    }
     l_run += rs;
     // O^T[d, query] += V^T P^T, V^T fragments by transposing reads of the V tile
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        const bf16x8 pb = acc_to_b(s[mt], hf);
+        const bf16x8 pb = acc_to_b(p[mt], hf);
 #pragma unroll
         for (int t = 0; t < C::DT; ++t)
           acc[t] = mfma32x32x16(frag_tr<DH>(vt, 32 * mt + 16 * hf, 32 * t, lane), pb, acc[t]);
@@ -164,14 +203,22 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
     __syncthreads();                  // stage j visible; every wave is done with stage j-1
     if (j + C::NS - 1 < ntiles) issue(j + C::NS - 1);   // into the slot of stage j-1
   };
+  constexpr std::true_type Y{};
+  constexpr std::false_type N{};
   int j = 0;
+  if (ntiles > 0) {                   // tile 0 holds key 0, which every query sees
+    step(0);
+    if (n_full > 0) tile(0, N, Y);
+    else tile(0, Y, Y);
+    j = 1;
+  }
   for (; j < n_full; ++j) {
     step(j);
-    tile(j, std::false_type{});
+    tile(j, N, N);
   }
   for (; j < ntiles; ++j) {
     step(j);
-    if (!(a.causal && 64 * j > qw + 31)) tile(j, std::true_type{});
+    if (!(a.causal && 64 * j > qw + 31)) tile(j, Y, N);
   }
 
   const float l_tot = sum_halves(l_run);

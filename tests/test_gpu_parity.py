@@ -88,6 +88,21 @@ def test_bf16_small_ragged(causal, S, H):
     compare_all(w, inp, gpu, Yr, g, "bf16", w.name)
 
 
+@pytest.mark.parametrize("causal", [True, False])
+def test_bf16_large_scores(causal):
+    """Scores far above the first key tile's maximum. Wq scaled by 16 (exact in bf16)
+    puts the scores' spread at ~23 octaves: the softmax is nearly one-hot and later key
+    tiles raise a row's maximum by more than 11 octaves hundreds of times (counted on
+    the oracle's Q, K), so the forward leaves its fast path and rescales."""
+    w = small_workload("bf16", B=1, S=700, D=256, H=2, F=512, causal=causal, Bq=128, Bkv=128)
+    inp = make_inputs(w, seed=7)
+    inp["Wq"] = (inp["Wq"].float() * 16).to(inp["Wq"].dtype)
+    say(f"case bf16 large scores {w.name}")
+    gpu = run_gpu(w, inp)
+    Yr, _, g = run_oracle(w, inp)
+    compare_all(w, inp, gpu, Yr, g, "bf16", w.name + "_x16")
+
+
 def test_bf16_saved_intermediates():
     """Kernel-level parity on what the forward saves: Q, K, V (projection GEMM),
     O and log-sum-exp (attention), h (output projection + residual), LN statistics."""
