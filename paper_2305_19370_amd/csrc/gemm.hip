@@ -122,13 +122,14 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
 }
 
 // Four consecutive columns n..n+3 of row m inside the stored width, from pointers
-// already at (m, n): c into C, r into R (EPI_RESID / EPI_MUL); c2 is the element index
-// of (m, n) in C2 (EPI_GELU); bn at bias[n]; bm = bias[m] for a per-row bias.
+// already at (m, n): c into C, r into R (EPI_RESID / EPI_MUL; for an fp32 C that
+// accumulates, the values of C already loaded); c2 is the element index of (m, n) in
+// C2 (EPI_GELU); bn at bias[n]; bm = bias[m] for a per-row bias.
 template <int EPI, typename CT, typename RT>
 BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const float* bn, float bm, f32x4 v) {
   if constexpr (EPI == EPI_STORE) {
     if constexpr (sizeof(CT) == 4) {
-      if (a.accumulate) v += V4<CT>::ld(c);
+      if (a.accumulate) v += V4<CT>::ld((const CT*)r);
     }
   } else if constexpr (EPI == EPI_RESID) {
     v += V4<RT>::ld((const RT*)r);
@@ -449,8 +450,43 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
   // wave, so no barrier is needed between strips.
   constexpr int PITCHF = Cfg::WN + 4;                // floats per staged row
   constexpr int C4 = Cfg::WN / 4;                    // 4-column groups per row
+  constexpr int RSTEP = 64 / C4;                     // rows per iteration of a strip
   float* strip = (float*)smem + wave * 32 * PITCHF;
   const bool inside = m0 + BM <= a.M && n0 + BN <= a.N;
+  // The operand the epilogue reads (R of a residual or multiplier epilogue, C itself
+  // for an fp32 C that accumulates) is loaded ahead for full tiles: 16-bit operands
+  // for all strips before the first staging, 32-bit ones two strips ahead, so that the
+  // load latency is not paid once per strip.
+  constexpr bool PRE = EPI == EPI_RESID || EPI == EPI_MUL || (EPI == EPI_STORE && sizeof(CT) == 4);
+  constexpr int PES = EPI == EPI_STORE ? (int)sizeof(CT) : (int)sizeof(RT);   // bytes per element
+  constexpr int PD = PES == 2 ? Cfg::TM : 2;                                   // strips in flight
+  constexpr int NIT = 32 / RSTEP;
+  typedef std::conditional_t<PES == 2, u32x2, u32x4> PreT;
+  PreT pre[PRE ? PD : 1][PRE ? NIT : 1];
+  const bool do_pre = PRE && inside && (EPI != EPI_STORE || a.accumulate);
+  const char* pbase = nullptr;
+  int64_t pld = 0;
+  if constexpr (PRE) {
+    const int64_t row0 = m0 + wm * Cfg::WM + lane / C4, col0 = n0 + wn * Cfg::WN + 4 * (lane % C4);
+    if constexpr (EPI == EPI_STORE) {
+      pbase = (const char*)((const CT*)a.C + z * a.sC + row0 * a.ldc + col0);
+      pld = a.ldc * PES;
+    } else {
+      pbase = (const char*)((const RT*)a.R + z * a.sR + row0 * a.ldr + col0);
+      pld = a.ldr * PES;
+    }
+  }
+  auto preload = [&](int i) {
+    if constexpr (PRE) {
+#pragma unroll
+      for (int it = 0; it < NIT; ++it)
+        pre[i % PD][it] = *(const PreT*)(pbase + (int64_t)(32 * i + RSTEP * it) * pld);
+    }
+  };
+  if (do_pre) {
+#pragma unroll
+    for (int i = 0; i < PD; ++i) preload(i);
+  }
 #pragma unroll
   for (int i = 0; i < Cfg::TM; ++i) {
 #pragma unroll
@@ -470,7 +506,6 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
       const int64_t c2b = z * a.sC2 + (mrow + r0) * a.ldc2 + ncol + c0;
       const float* bb = a.bias ? a.bias + ncol + c0 : nullptr;
       constexpr int RS = (int)sizeof(RT);
-      constexpr int RSTEP = 64 / C4;                 // rows per iteration
       // the GELU epilogue is long: keep its loop rolled (instruction cache)
       constexpr int UNR = EPI == EPI_GELU ? 4 : 32 / RSTEP;
 #pragma unroll UNR
@@ -478,10 +513,14 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
         const int row = r0 + RSTEP * it;
         const f32x4 v = *(const f32x4*)(strip + row * PITCHF + c0);
         const float bm = (EPI == EPI_GELU && a.bias && a.bias_on_m) ? a.bias[mrow + row] : 0.0f;
-        epi_vec4<EPI, CT, RT>(a, cb + (int64_t)RSTEP * it * a.ldc,
-                              rb + (int64_t)RSTEP * it * a.ldr * RS,
-                              c2b + (int64_t)RSTEP * it * a.ldc2, bb, bm, v);
+        if constexpr (PRE)
+          epi_vec4<EPI, CT, RT>(a, cb + (int64_t)RSTEP * it * a.ldc, &pre[i % PD][it], 0, bb, bm, v);
+        else
+          epi_vec4<EPI, CT, RT>(a, cb + (int64_t)RSTEP * it * a.ldc,
+                                rb + (int64_t)RSTEP * it * a.ldr * RS,
+                                c2b + (int64_t)RSTEP * it * a.ldc2, bb, bm, v);
       }
+      if (do_pre && i + PD < Cfg::TM) preload(i + PD);
     } else {
 #pragma unroll 1
       for (int e = lane; e < 32 * C4; e += 64) {
