@@ -87,7 +87,8 @@ typedef struct {           /* fp32 device pointers, overwritten; NULL = not want
 /* Byte offsets of the tensors the forward saves for the backward, inside the
  * caller's `saved` buffer. E = element size of cfg->dtype; T = B*S tokens;
  * Sp = S rounded up to a multiple of 64.
- *   qkv  [T, 3D] E   Q (unscaled) in columns [0, D), K in [D, 2D), V in [2D, 3D)
+ *   qkv  [T, 3D] E   Q in columns [0, D) (dtype BF16: multiplied by log2(e)/sqrt(D/H),
+ *                    the base-2 score scale; F32: unscaled), K in [D, 2D), V in [2D, 3D)
  *   o    [T, D] E    attention output (heads concatenated), before Wo
  *   lse  [B, H, Sp] fp32  natural-log log-sum-exp of each query row's scores
  *   h    [T, D] fp32 residual stream after attention, X + O Wo

@@ -10,7 +10,10 @@ namespace bpt {
 // MFMAs) of 32 keys each, 256 keys per workgroup, loop over query tiles of 64 (two
 // halves of 32). S = Q K^T and dP = dO V^T have the key on the lane axis, so P and dS
 // feed dV^T += dO^T P and dK^T += Q^T dS directly as B operands; dO^T and Q^T
-// fragments come from the token-major tiles by transposing LDS reads.
+// fragments come from the token-major tiles by transposing LDS reads. Q carries
+// log2(e)/sqrt(dh), and the score MFMAs start from minus the base-2 log-sum-exp of
+// their query rows, so exp2 of the accumulator is P; dK = sqrt(dh)^-1 dS^T Q then
+// comes out as ln(2) dS^T (Q log2(e)/sqrt(dh)).
 // Query tiles are visited from the last one down, so all workgroups of a head start
 // on the same tiles (and share them in L2); the diagonal tiles come last.
 template <int DH>
@@ -19,7 +22,7 @@ struct DkvCfg {
   static constexpr int NW = 8;                      // waves per workgroup
   static constexpr int KEYS = 32 * NW;              // keys per workgroup
   static constexpr int TB = RmTile<DH>::BYTES;
-  static constexpr int STAGE = 2 * TB + 2 * 64 * 4; // Q, dO tiles; lse (base 2), -Delta
+  static constexpr int STAGE = 2 * TB + 2 * 64 * 4; // Q, dO tiles; -lse (base 2), -Delta
   static constexpr int NS = 4;                      // stages in the ring
   static constexpr int LDS = NS * STAGE;
   static constexpr int DPS = Ring2<DH, NW>::DPW + 2;  // copies per wave per stage
@@ -40,13 +43,12 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
   const int kw = k0 + 32 * wave;                    // first key of this wave
   const int key = kw + (lane & 31);
   const float scale = rsqrtf((float)DH);
-  const float c = scale * LOG2E;
 
   const bf16* Qb = (const bf16*)a.q + (int64_t)b * a.S * a.ld_q + h * DH;
   const bf16* Kb = (const bf16*)a.k + (int64_t)b * a.S * a.ld_k + h * DH;
   const bf16* Vb = (const bf16*)a.v + (int64_t)b * a.S * a.ld_v + h * DH;
   const bf16* dOb = (const bf16*)a.dout + (int64_t)b * a.S * a.ld_do + h * DH;
-  const float* lse2 = a.lse2 + ((int64_t)b * a.H + h) * a.Sp;
+  const float* nlse2 = a.nlse2 + ((int64_t)b * a.H + h) * a.Sp;
   const float* ndelta = a.ndelta + ((int64_t)b * a.H + h) * a.Sp;
 
   bf16x8 kf[C::KSTEPS], vf[C::KSTEPS];
@@ -69,9 +71,9 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     const int qt0 = qstart + 64 * (ntiles - 1 - it);
     char* st = smem + (it % C::NS) * C::STAGE;
     ring_issue<DH, C::NW>(st, Qb, (int)a.ld_q, qt0, dOb, (int)a.ld_do, qt0, S - 1, wave, lane);
-    // base-2 lse and -Delta of the 64 queries (indices < Sp: in bounds; rows >= S are
+    // -lse (base 2) and -Delta of the 64 queries (indices < Sp: in bounds; rows >= S are
     // masked); every wave copies them, so that all waves count the same copies
-    dma4s(lse2 + qt0, 4u * lane, st + 2 * C::TB);
+    dma4s(nlse2 + qt0, 4u * lane, st + 2 * C::TB);
     dma4s(ndelta + qt0, 4u * lane, st + 2 * C::TB + 256);
   };
 
@@ -93,15 +95,20 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     const int lo4 = lo - 4 * (lane >> 5), hi4 = hi - 4 * (lane >> 5);
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      // dP starts from -Delta of its query rows, so the MFMAs leave dP - Delta
-      f32x16 dp;
+      // S starts from -lse and dP from -Delta of their query rows, so the MFMAs leave
+      // the exponent of P and dP - Delta
+      f32x16 s, dp;
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
-        const f32x4 d4 = *(const f32x4*)(ls + 64 + 32 * mt + 8 * rg + 4 * (lane >> 5));
+        const int qi = 32 * mt + 8 * rg + 4 * (lane >> 5);
+        const f32x4 l4 = *(const f32x4*)(ls + qi);
+        const f32x4 d4 = *(const f32x4*)(ls + 64 + qi);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) dp[4 * rg + e] = d4[e];    // -Delta as stored
+        for (int e = 0; e < 4; ++e) {
+          s[4 * rg + e] = l4[e];
+          dp[4 * rg + e] = d4[e];
+        }
       }
-      f32x16 s = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < C::KSTEPS; ++kk) {
         s = mfma32x32x16(frag_rows<DH>(qs, 32 * mt, 2 * kk, lane), kf[kk], s);
@@ -110,12 +117,10 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
       }
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
-        const int qi = 32 * mt + 8 * rg + 4 * (lane >> 5);
-        const f32x4 l4 = *(const f32x4*)(ls + qi);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * rg + e;
-          float p = fast_exp2(fmaf(s[r], c, -l4[e]));
+          float p = fast_exp2(s[r]);
           if constexpr (decltype(MASK)::value) {
             const int off = 32 * mt + 8 * rg + e;
             p = (off >= lo4 && off <= hi4) ? p : 0.0f;
@@ -179,7 +184,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t d = 32 * t + acc_row(r, lane);
-        dKt[d * a.ld_dt] = (bf16)(adk[t][r] * scale);
+        dKt[d * a.ld_dt] = (bf16)(adk[t][r] * LN2);
         dVt[d * a.ld_dt] = (bf16)adv[t][r];
       }
   }

@@ -9,7 +9,9 @@ namespace bpt {
 // Query-outer: 8 waves (two per SIMD, so one wave's VALU work overlaps the other's
 // MFMAs) of 32 queries each, 256 per workgroup, loop over key tiles of 64:
 // S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - Delta), dQ^T += K^T dS^T. K^T
-// fragments come from the K tile by transposing LDS reads.
+// fragments come from the K tile by transposing LDS reads. Q carries log2(e)/sqrt(dh),
+// and the score MFMAs start from minus the base-2 log-sum-exp of the lane's query, so
+// exp2 of the accumulator is P.
 template <int DH>
 struct DqCfg {
   static constexpr int KSTEPS = DH / 16, DT = DH / 32;
@@ -38,7 +40,6 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
   const int qw = q0 + 32 * wave;
   const int qrow = qw + (lane & 31);
   const float scale = rsqrtf((float)DH);
-  const float c = scale * LOG2E;
 
   const bf16* Qb = (const bf16*)a.q + (int64_t)b * a.S * a.ld_q + h * DH;
   const bf16* Kb = (const bf16*)a.k + (int64_t)b * a.S * a.ld_k + h * DH;
@@ -56,7 +57,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
     settle(dof[kk]);
   }
   const int64_t sidx = ((int64_t)b * a.H + h) * a.Sp + qr;
-  const float nlse2 = qok ? -a.lse2[sidx] : 0.0f;
+  const float nlse2 = qok ? a.nlse2[sidx] : 0.0f;
   const float ndl = qok ? a.ndelta[sidx] : 0.0f;   // -Delta
   settle(nlse2);
   settle(ndl);
@@ -81,9 +82,12 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
     const char* vt = kt + C::TB;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      f32x16 s = f32x16{}, dp;
+      f32x16 s, dp;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dp[r] = ndl;     // the MFMAs leave dP^T - Delta
+      for (int r = 0; r < 16; ++r) {
+        s[r] = nlse2;                                // the MFMAs leave the exponent of P
+        dp[r] = ndl;                                 // and dP^T - Delta
+      }
 #pragma unroll
       for (int kk = 0; kk < C::KSTEPS; ++kk) {
         s = mfma32x32x16(frag_rows<DH>(kt, 32 * mt, 2 * kk, lane), qf[kk], s);
@@ -94,7 +98,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
       const int lim = kv_last - kv0 - 32 * mt - 4 * (lane >> 5);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float p = fast_exp2(fmaf(s[r], c, nlse2));
+        float p = fast_exp2(s[r]);
         if constexpr (decltype(MASK)::value) p = (8 * (r >> 2) + (r & 3) <= lim) ? p : 0.0f;
         s[r] = p * dp[r];                           // dS^T
       }

@@ -11,6 +11,7 @@
 namespace bpt {
 
 static constexpr float LOG2E = 1.4426950408889634f;
+static constexpr float LN2 = 0.6931471805599453f;
 static constexpr float NEG_INF = -__builtin_inff();
 
 // Row-major LDS tile: 64 token rows of DH bf16 features. The pitch (DH*2 + 48 bytes

@@ -15,8 +15,11 @@
 //    through a 4-stage LDS ring filled by direct global->LDS copies; V^T fragments
 //    come from the V tile by transposing LDS reads;
 //  * 8 waves of 32 queries share each stage; two waves per SIMD let one wave's
-//    softmax run while the other's MFMAs do; scores use exp2 with log2(e)/sqrt(dh)
-//    folded in one FMA.
+//    softmax run while the other's MFMAs do;
+//  * Q arrives multiplied by log2(e)/sqrt(dh) (the projection's epilogue applies it),
+//    so scores are base-2 logits, and the score MFMAs start from minus the row's
+//    reference maximum: exp2 of the accumulator is the weight, and the backward
+//    kernels start them from minus the base-2 log-sum-exp in the same way.
 // fp32 kernels: one query (or key) row per thread with VALU FMAs; used by the
 // fp32 parity workload.
 #include <algorithm>
@@ -63,8 +66,6 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
   const int q0 = (int)a.q_begin + qt * C::QROWS;
   const int qw = q0 + 32 * wave;                    // first query of this wave
   const int qrow = qw + (lane & 31);
-  const float scale = rsqrtf((float)DH);
-  const float c = scale * LOG2E;
 
   const bf16* Qb = (const bf16*)a.q + (int64_t)b * a.S * a.ld_q + h * DH;
   const bf16* Kb = (const bf16*)a.k + (int64_t)b * a.S * a.ld_k + h * DH;
@@ -92,49 +93,55 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
   f32x16 acc[C::DT];                                // O^T of the wave's queries
 #pragma unroll
   for (int t = 0; t < C::DT; ++t) acc[t] = f32x16{};
-  float m_run = NEG_INF, l_run = 0.0f;
+  // Q carries log2(e)/sqrt(dh), so the scores are base-2 logits. ref is the row's
+  // reference maximum (base 2); the score MFMAs start from -ref, so that they leave
+  // score - ref, the exponent of the weight, with no VALU work per score.
+  float ref = 0.0f, l_run = 0.0f;
+  f32x16 sinit = f32x16{};
 
-  // Rescale the running numerator and sum to a new reference maximum mx (per lane);
-  // lanes whose maximum grew by at most RESCALE_LOG2 keep their reference.
-  auto rescale = [&](float mx) {
-    const bool up = (mx - m_run) * c > RESCALE_LOG2;      // true on the first visible tile
-    if (__ballot(up)) {
-      asm volatile("" ::: "memory");                       // keep the rescale behind the branch
-      const float corr = up ? fast_exp2((m_run - mx) * c) : 1.0f;   // exp2(-inf) = 0
-      l_run *= corr;
-#pragma unroll
-      for (int t = 0; t < C::DT; ++t) acc[t] *= corr;
-    }
-    if (up) m_run = mx;
-  };
-  auto row_max = [&](const f32x16 (&s)[2]) {
-    float mx = NEG_INF;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
-    return max_halves(mx);
-  };
-  // exp-weights of the tile against the current reference maximum, and their sum
-  auto weights = [&](const f32x16 (&s)[2], f32x16 (&p)[2]) {
-    const float mc = (m_run == NEG_INF ? 0.0f : m_run) * c;
+  // Weights exp2(t - d) of the tile's exponents t = score - ref, with d = 0 or d the
+  // lane's maximum of t (shared with lane ^ 32); their sum over the lane's 32 keys.
+  auto weights = [&](const f32x16 (&t)[2], float d, f32x16 (&p)[2]) {
     float rs = 0.0f;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        p[mt][r] = fast_exp2(fmaf(s[mt][r], c, -mc));
+        p[mt][r] = fast_exp2(t[mt][r] - d);
         rs += p[mt][r];
       }
     return rs;
   };
+  auto tile_max = [&](const f32x16 (&t)[2]) {
+    float mx = NEG_INF;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, t[mt][r]);
+    return max_halves(mx);
+  };
+  // Move the reference up by d (per lane) and rescale numerator and sum to it.
+  auto move_ref = [&](float d) {
+    if (__ballot(d != 0.0f)) {
+      asm volatile("" ::: "memory");                       // keep the rescale behind the branch
+      const float corr = fast_exp2(-d);
+      l_run *= corr;
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t) acc[t] *= corr;
+      ref += d;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sinit[r] = -ref;
+    }
+  };
 
-  // EXACT: the reference maximum follows the tile's row maximum (the first tile of
-  // every wave, which sets a finite reference on every row). Otherwise the weights are
-  // taken against the current reference first, and the maximum is only computed when
-  // a lane's sum of weights exceeds SUM_MAX (a score above the reference by more than
-  // about log2(SUM_MAX / 32) / c); every weight then stays <= SUM_MAX, and no row sum can
-  // vanish because the first tile left a weight of 1 at its maximum.
+  // EXACT: the tile sets the reference to its row maximum (the first tile of every
+  // wave: it holds key 0, which every query sees, so every reference ends up finite).
+  // Otherwise the weights are taken against the current reference directly, and the
+  // tile maximum is only computed when a lane's sum of weights exceeds SUM_MAX (a
+  // score above the reference by more than about log2(SUM_MAX / 32)); the reference
+  // then moves when the maximum is above it by more than RESCALE_LOG2. Every weight
+  // stays <= SUM_MAX, and no row sum can vanish, the first tile having left a weight
+  // of 1 at its maximum.
   auto tile = [&](int j, auto MASK, auto EXACT) {
     const int kv0 = 64 * j;
     const char* kt = smem + (j % C::NS) * C::STAGE;
@@ -146,12 +153,12 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) kf[kk][mt] = frag_rows<DH>(kt, 32 * mt, 2 * kk, lane);
     __builtin_amdgcn_sched_barrier(0);
-    // S^T[key, query] = K Q^T
-    f32x16 s[2] = {f32x16{}, f32x16{}};
+    // T^T[key, query] = K Q^T - ref
+    f32x16 t[2] = {sinit, sinit};
 #pragma unroll
     for (int kk = 0; kk < C::KSTEPS; ++kk)
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) s[mt] = mfma32x32x16(kf[kk][mt], qf[kk], s[mt]);
+      for (int mt = 0; mt < 2; ++mt) t[mt] = mfma32x32x16(kf[kk][mt], qf[kk], t[mt]);
     if constexpr (decltype(MASK)::value) {
       // key offset of register r: 32 mt + acc_row(r, lane); the lane part moves into the
       // limit so that every comparison is against a constant
@@ -159,19 +166,24 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s[mt][r] = (32 * mt + 8 * (r >> 2) + (r & 3) <= lim) ? s[mt][r] : NEG_INF;
+        for (int r = 0; r < 16; ++r) t[mt][r] = (32 * mt + 8 * (r >> 2) + (r & 3) <= lim) ? t[mt][r] : NEG_INF;
     }
     f32x16 p[2];
     float rs;
     if constexpr (decltype(EXACT)::value) {
-      rescale(row_max(s));
-      rs = weights(s, p);
+      const float mx = tile_max(t);                        // finite: key 0 is in this tile
+      ref += mx;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sinit[r] = -ref;
+      rs = weights(t, mx, p);
     } else {
-      rs = weights(s, p);
+      rs = weights(t, 0.0f, p);
       if (__ballot(!(rs <= SUM_MAX))) {
         asm volatile("" ::: "memory");
-        rescale(row_max(s));
-        rs = weights(s, p);
+        const float mx = tile_max(t);
+        const float d = mx > RESCALE_LOG2 ? mx : 0.0f;
+        move_ref(d);
+        rs = weights(t, d, p);
       }
     }
     l_run += rs;
@@ -182,8 +194,8 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
       for (int hf = 0; hf < 2; ++hf) {
         const bf16x8 pb = acc_to_b(p[mt], hf);
 #pragma unroll
-        for (int t = 0; t < C::DT; ++t)
-          acc[t] = mfma32x32x16(frag_tr<DH>(vt, 32 * mt + 16 * hf, 32 * t, lane), pb, acc[t]);
+        for (int t2 = 0; t2 < C::DT; ++t2)
+          acc[t2] = mfma32x32x16(frag_tr<DH>(vt, 32 * mt + 16 * hf, 32 * t2, lane), pb, acc[t2]);
       }
   };
 
@@ -234,7 +246,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
         for (int e = 0; e < 4; ++e) v[e] = (bf16)(acc[t][4 * rg + e] * inv);
         *(bf16x4*)(Op + 32 * t + 8 * rg + 4 * (lane >> 5)) = v;
       }
-    if (lane < 32) a.lse[((int64_t)b * a.H + h) * a.Sp + qrow] = m_run * scale + logf(l_tot);
+    if (lane < 32) a.lse[((int64_t)b * a.H + h) * a.Sp + qrow] = (ref + log2f(l_tot)) * LN2;
   }
 }
 

@@ -41,6 +41,7 @@ BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float
     return;
   }
   if constexpr (EPI == EPI_STORE) {
+    v *= a.alpha;
     if constexpr (sizeof(CT) == 4) {
       if (a.accumulate) v += to_f32<CT>(C[idx]);
     }
@@ -95,6 +96,7 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
   }
   CT* C = (CT*)a.C + z * a.sC + m * a.ldc + n;
   if constexpr (EPI == EPI_STORE) {
+    v *= a.alpha;
     if constexpr (sizeof(CT) == 4) {
       if (a.accumulate) v += V4<CT>::ld(C);
     }
@@ -128,6 +130,7 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
 template <int EPI, typename CT, typename RT>
 BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const float* bn, float bm, f32x4 v) {
   if constexpr (EPI == EPI_STORE) {
+    v *= a.alpha;
     if constexpr (sizeof(CT) == 4) {
       if (a.accumulate) v += V4<CT>::ld((const CT*)r);
     }

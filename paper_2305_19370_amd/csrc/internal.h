@@ -33,6 +33,7 @@ struct GemmArgs {
   int64_t sA = 0, sB = 0, sC = 0, sR = 0, sC2 = 0;   // batch strides in elements
   int batch = 1;
   int accumulate = 0;          // fp32 C only: C += acc
+  float alpha = 1.0f;          // EPI_STORE: acc is multiplied by alpha before it is stored
   int bias_on_m = 0;           // EPI_GELU: bias indexed by row instead of column
   // Transposed operands (trans_b with any epilogue, trans_a with EPI_STORE or EPI_GELU,
   // both with EPI_STORE): trans_a means A is stored K-major, element
@@ -49,6 +50,9 @@ struct GemmArgs {
 hipError_t gemm(Dt ab, Epi epi, Dt ct, Dt rt, const GemmArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- attention
+// The bf16 kernels take Q multiplied by log2(e)/sqrt(dh), so that Q K^T are the scores in
+// base-2 units (exp2 of them is the unnormalised probability); the fp32 kernels take Q
+// as the projection produced it.
 struct AttnArgs {
   // token-major tensors: token (b, s) is row b*S + s
   const void* q = nullptr;  int64_t ld_q = 0;    // pointer already at head 0's first column
@@ -60,7 +64,7 @@ struct AttnArgs {
   void* dqt = nullptr; void* dkt = nullptr; void* dvt = nullptr; int64_t ld_dt = 0;
   float* lse = nullptr;        // [B, H, Sp] natural log
   const float* ndelta = nullptr;// [B, H, Sp] -Delta, Delta = rowsum(dO * O)
-  const float* lse2 = nullptr; // [B, H, Sp] log-sum-exp in base 2 (backward)
+  const float* nlse2 = nullptr;// [B, H, Sp] minus the log-sum-exp in base 2 (bf16 backward)
   int64_t S = 0, Sp = 0;
   int B = 0, H = 0, dh = 0;
   int causal = 0;
@@ -108,9 +112,9 @@ hipError_t col_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols,
 hipError_t row_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols, float* out,
                    int accumulate, hipStream_t s);
 
-// ndelta[b, h, s] = -sum_d dO[b*S+s, h*dh+d] * O[b*S+s, h*dh+d]; lse2 = lse * log2(e);
+// ndelta[b, h, s] = -sum_d dO[b*S+s, h*dh+d] * O[b*S+s, h*dh+d]; nlse2 = -lse * log2(e);
 // both are 0 for the padding positions s >= S
 hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, const float* lse, float* ndelta,
-                      float* lse2, int B, int64_t S, int64_t Sp, int H, int dh, hipStream_t s);
+                      float* nlse2, int B, int64_t S, int64_t Sp, int H, int dh, hipStream_t s);
 
 }  // namespace bpt

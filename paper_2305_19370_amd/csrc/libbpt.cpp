@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 #include <map>
 #include <mutex>
 #include <string>
@@ -136,7 +137,7 @@ struct BwdWs {
   void *wcat;
   void *vg, *gT, *dzT;
   void* gpT;             // GELU'(Z^T): fp32 on the fp32 path, fp16 on the bf16 path
-  float *dv, *dh, *dU, *ndelta, *lse2, *partial, *scratch;
+  float *dv, *dh, *dU, *ndelta, *nlse2, *partial, *scratch;
   void *dhe, *dhT, *dO, *dqkvT, *u;
 };
 
@@ -154,7 +155,7 @@ BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
   w.dhT = bp.take(d.D * d.Tp * d.E);
   w.dO = bp.take(d.T * d.D * d.E);
   w.ndelta = (float*)bp.take(d.B * d.H * d.Sp * 4);
-  w.lse2 = (float*)bp.take(d.B * d.H * d.Sp * 4);
+  w.nlse2 = (float*)bp.take(d.B * d.H * d.Sp * 4);
   w.dqkvT = bp.take(3 * d.D * d.Tp * d.E);
   w.u = bp.take(d.T * d.D * d.E);
   w.dU = (float*)bp.take(d.T * d.D * 4);
@@ -381,6 +382,8 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
   for (int i = 0; i < 3; ++i) {
     GemmArgs g;
     g.A = w.u; g.lda = D; g.B = wqkv[i]; g.ldb = D; g.trans_b = 1;
+    // bf16 attention takes Q multiplied by log2(e)/sqrt(dh): scores in base-2 units
+    if (i == 0 && E == BF16) g.alpha = (float)(1.4426950408889634 / std::sqrt((double)d.dh));
     g.C = off(sv.qkv, i * D * E_); g.ldc = 3 * D; g.M = T; g.N = D; g.K = D;
     RUN("gemm.qkv", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
   }
@@ -547,7 +550,7 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
   }
 
   // ---- attention backward, probabilities rebuilt from the saved log-sum-exp
-  RUN("attn.delta", 0, 2.0 * T * D * E_, attn_delta(E, w.dO, sv.o, D, sv.lse, w.ndelta, w.lse2, B, S, Sp, (int)d.H, (int)d.dh, s));
+  RUN("attn.delta", 0, 2.0 * T * D * E_, attn_delta(E, w.dO, sv.o, D, sv.lse, w.ndelta, w.nlse2, B, S, Sp, (int)d.H, (int)d.dh, s));
   {
     AttnArgs a;
     a.q = sv.qkv; a.ld_q = 3 * D;
@@ -555,7 +558,7 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     a.v = off(sv.qkv, 2 * D * E_); a.ld_v = 3 * D;
     a.dout = w.dO; a.ld_do = D;
     a.dqt = w.dqkvT; a.dkt = off(w.dqkvT, D * Tp * E_); a.dvt = off(w.dqkvT, 2 * D * Tp * E_); a.ld_dt = Tp;
-    a.lse = sv.lse; a.ndelta = w.ndelta; a.lse2 = w.lse2;
+    a.lse = sv.lse; a.ndelta = w.ndelta; a.nlse2 = w.nlse2;
     a.S = S; a.Sp = Sp; a.B = B; a.H = (int)d.H; a.dh = (int)d.dh; a.causal = cfg->causal;
     const double pairs = attn_pairs(0, S, S, cfg->causal) * d.H * B;
     // key-outer: S = Q K^T, dP = dO V^T, dV += P^T dO, dK += dS^T Q (4 contractions)

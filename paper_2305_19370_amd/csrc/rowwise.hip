@@ -311,10 +311,11 @@ __global__ __launch_bounds__(256) void row_sum_kernel(const T* in, int64_t ld, i
 // One wave per token (b, s): Delta[b, h, s] = sum_d dO[t, h*dh + d] O[t, h*dh + d] for every
 // head, from 16-byte loads of the token's two rows; the lanes of one head reduce by
 // shuffles; stored negated (the backward kernels start dP from -Delta). Also
-// lse2 = lse * log2(e). Padding tokens s in [S, Sp) get zeros.
+// nlse2 = -lse * log2(e), the negated base-2 log-sum-exp. Padding tokens s in [S, Sp) get
+// zeros.
 template <typename T>
 __global__ __launch_bounds__(256) void delta_kernel(const T* dO, const T* O, int64_t ld, const float* lse,
-                                                    float* ndelta, float* lse2, int B, int64_t S, int64_t Sp,
+                                                    float* ndelta, float* nlse2, int B, int64_t S, int64_t Sp,
                                                     int H, int dh) {
   constexpr int EPL = 16 / sizeof(T);                // elements per lane and load
   const int lane = threadIdx.x & 63;
@@ -342,7 +343,7 @@ __global__ __launch_bounds__(256) void delta_kernel(const T* dO, const T* O, int
       const int h = e / dh;
       const int64_t i = ((int64_t)b * H + h) * Sp + s;
       ndelta[i] = -acc;
-      lse2[i] = s < S ? lse[i] * 1.4426950408889634f : 0.0f;
+      nlse2[i] = s < S ? -lse[i] * 1.4426950408889634f : 0.0f;
     }
   }
 }
@@ -480,12 +481,12 @@ hipError_t row_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols,
 }
 
 hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, const float* lse, float* ndelta,
-                      float* lse2, int B, int64_t S, int64_t Sp, int H, int dh, hipStream_t s) {
+                      float* nlse2, int B, int64_t S, int64_t Sp, int H, int dh, hipStream_t s) {
   // one wave per token; a head spans whole 16-byte loads
   const int64_t n = (int64_t)B * Sp;
   if (dh % (t == F32 ? 4 : 8) != 0) return hipErrorInvalidValue;
   BPT_T(t, T, hipLaunchKernelGGL((delta_kernel<T>), dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s,
-                                 (const T*)dout, (const T*)o, ld, lse, ndelta, lse2, B, S, Sp, H, dh));
+                                 (const T*)dout, (const T*)o, ld, lse, ndelta, nlse2, B, S, Sp, H, dh));
   return hipGetLastError();
 }
 

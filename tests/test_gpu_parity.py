@@ -14,6 +14,8 @@ with ref the float64 oracle):
         decides; the weight gradients and, with the causal mask, dX carry the
         bf16 floor above 2e-2 / 2e-3.
 """
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -115,8 +117,10 @@ def test_bf16_saved_intermediates():
     B, S, D, H = w.B, w.S, w.D, w.H
     Sp = (S + 63) // 64 * 64
     qkv = sv["qkv"]
+    # the bf16 path stores Q multiplied by log2(e)/sqrt(dh) (the scores' base-2 scale)
+    qscale = math.log2(math.e) / math.sqrt(D // H)
     checks = {
-        "Q": (qkv[:, :D].reshape(B, S, D), c["Q"]),
+        "Q": (qkv[:, :D].reshape(B, S, D) / qscale, c["Q"]),
         "K": (qkv[:, D:2 * D].reshape(B, S, D), c["K"]),
         "V": (qkv[:, 2 * D:].reshape(B, S, D), c["V"]),
         "O": (sv["o"].reshape(B, S, D), c["O"]),
