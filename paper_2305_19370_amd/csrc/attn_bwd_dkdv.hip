@@ -35,14 +35,12 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int S = (int)a.S;
-  const int nblk = (S + C::KEYS - 1) / C::KEYS;
   int hh, blk;
-  xcd_map((int)blockIdx.x, nblk, a.H * a.B, hh, blk);
+  xcd_map((int)blockIdx.x, a.H * a.B, hh, blk);
   const int h = hh % a.H, b = hh / a.H;
   const int k0 = blk * C::KEYS;                     // causal: low key blocks have the most queries
   const int kw = k0 + 32 * wave;                    // first key of this wave
   const int key = kw + (lane & 31);
-  const float scale = rsqrtf((float)DH);
 
   const bf16* Qb = (const bf16*)a.q + (int64_t)b * a.S * a.ld_q + h * DH;
   const bf16* Kb = (const bf16*)a.k + (int64_t)b * a.S * a.ld_k + h * DH;

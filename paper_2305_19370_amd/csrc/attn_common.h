@@ -208,11 +208,11 @@ BPT_DEV void drain_all(f32x16 (&a)[DT]) {
 // Row of accumulator register r for lane `lane` inside a 32x32 tile.
 BPT_DEV int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
-// Workgroup id -> (head instance hh in [0, NH), block in [0, nblk)). Workgroup i runs
+// Workgroup id -> (head instance hh in [0, NH), block index blk). Workgroup i runs
 // on XCD i % 8 and every XCD has its own L2; when NH is a multiple of 8, all blocks of
 // a head run on one XCD, so the blocks that stream the same K/V (or Q/dO) tiles share
 // that L2. Block 0 of every head is dispatched first.
-BPT_DEV void xcd_map(int id, int nblk, int NH, int& hh, int& blk) {
+BPT_DEV void xcd_map(int id, int NH, int& hh, int& blk) {
   if ((NH & 7) == 0) {
     const int x = id & 7, k = id >> 3, hp = NH >> 3;
     hh = x + 8 * (k % hp);

@@ -60,7 +60,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_bf16_kernel(AttnArgs a) {
   const int S = (int)a.S;
   const int nblk = (int)((a.q_end - a.q_begin + C::QROWS - 1) / C::QROWS);
   int hh, blk;
-  xcd_map((int)blockIdx.x, nblk, a.H * a.nb, hh, blk);
+  xcd_map((int)blockIdx.x, a.H * a.nb, hh, blk);
   const int h = hh % a.H, b = a.b_begin + hh / a.H;
   const int qt = a.causal ? nblk - 1 - blk : blk;   // causal: the blocks with the most keys first
   const int q0 = (int)a.q_begin + qt * C::QROWS;

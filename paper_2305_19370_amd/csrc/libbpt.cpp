@@ -205,11 +205,9 @@ hipError_t launch(const char* name, double flops, double bytes, hipStream_t s, F
   if (!g_prof_on) return fn();
   std::lock_guard<std::mutex> lk(g_prof_mu);
   hipEvent_t a = pool_event(), b = pool_event();
-  if (!a || !b) return fn();
-  hipEventRecord(a, s);
+  if (!a || !b || hipEventRecord(a, s) != hipSuccess) return fn();
   hipError_t e = fn();
-  hipEventRecord(b, s);
-  g_prof.push_back({name, flops, bytes, a, b});
+  if (hipEventRecord(b, s) == hipSuccess) g_prof.push_back({name, flops, bytes, a, b});
   return e;
 }
 

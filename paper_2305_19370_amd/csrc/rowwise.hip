@@ -373,7 +373,7 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* in, int64_t ld_
 
 template <typename T>
 __global__ __launch_bounds__(256) void copy2d_kernel(const T* in, int64_t ld_in, T* out, int64_t ld_out,
-                                                     int64_t rows, int64_t cols) {
+                                                     int64_t cols) {   // one row per grid row
   const int64_t r = blockIdx.y;
   for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < cols; c += (int64_t)gridDim.x * 256)
     out[r * ld_out + c] = in[r * ld_in + c];
@@ -505,7 +505,7 @@ hipError_t copy2d(Dt t, const void* in, int64_t ld_in, void* out, int64_t ld_out
   if (rows <= 0 || cols <= 0) return hipSuccess;
   const unsigned gx = (unsigned)((cols + 255) / 256 < 64 ? (cols + 255) / 256 : 64);
   BPT_T(t, T, hipLaunchKernelGGL((copy2d_kernel<T>), dim3(gx, (unsigned)rows), dim3(256), 0, s,
-                                 (const T*)in, ld_in, (T*)out, ld_out, rows, cols));
+                                 (const T*)in, ld_in, (T*)out, ld_out, cols));
   return hipGetLastError();
 }
 
