@@ -27,6 +27,10 @@ Contents
                from the exact result on a given input (tolerance floor).
 ``bf16_rows``  ``bf16_model`` restricted to selected query rows, like ``rows``
                (the tolerance floor at full workload sizes).
+``xent``       Cross-entropy of a language-model head (Section 3's remark that
+               the blockwise scheme applies to the final loss): the plain,
+               unblocked logits h W, log-sum-exp, mean token loss and its
+               gradients dh, dW.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against brute-force
 loops, closed forms, invariants, finite differences and an independent
