@@ -128,3 +128,21 @@ def small_workload(dtype: str = "f32", B: int = 1, S: int = 250, D: int = 256, H
     return Workload(f"small_{dtype}_B{B}_S{S}_D{D}_H{H}_F{F}_{'c' if causal else 'nc'}",
                     B, S, D, H, F, causal, Bq, Bkv, dtype,
                     init or ("small" if dtype == "f32" else "unit"))
+
+
+# ---------------------------------------------------------------- LM-head cross-entropy inputs
+def make_xent_inputs(T: int, D: int, V: int, ldw: int, dtype: str = "bf16", seed: int = 0,
+                     logit_std: float = 2.0) -> Dict[str, torch.Tensor]:
+    """Inputs of the LM-head cross-entropy, CPU tensors: h [T, D] ~ N(0, 1) (a final
+    LayerNorm's output), W [D, ldw] ~ N(0, logit_std^2 / D) in its first V columns and
+    zero in the padding columns (so logits have std ~logit_std), targets [T] int32
+    uniform over [0, V). One CPU generator, draws in the order h, W, targets; h and W
+    rounded once to the storage dtype."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    dt = torch_dtype(dtype)
+    h = torch.randn((T, D), generator=g, dtype=torch.float32).to(dt)
+    W = torch.zeros((D, ldw), dtype=torch.float32)
+    W[:, :V] = torch.randn((D, V), generator=g, dtype=torch.float32) * (logit_std / D ** 0.5)
+    targets = torch.randint(0, V, (T,), generator=g, dtype=torch.int32)
+    return {"h": h, "W": W.to(dt), "targets": targets}

@@ -144,6 +144,54 @@ size_t bpt_describe(const bpt_config* cfg, char* buf, size_t buf_bytes);
 bpt_status bpt_profile_enable(int on);
 size_t bpt_profile_report(char* buf, size_t buf_bytes);
 
+/* ---------------------------------------------------------------------------
+ * Cross-entropy of a language-model head, blockwise over tokens. Section 3 of the
+ * paper remarks that the blockwise scheme applies to the final cross-entropy loss
+ * as well: here the [T, V] logits never exist at once, only those of block_rows
+ * tokens, in the workspace.
+ *
+ *     logits = h W        h [T, D] and W [D, ldw] in cfg->dtype (row-major, y = x @ W);
+ *                         the first V columns of W are the vocabulary
+ *     lse_t  = log sum_{v < V} exp(logits[t, v])
+ *     loss   = (1/T) sum_t (lse_t - logits[t, y_t])
+ *
+ * The backward recomputes each block's logits and forms G = (dloss / T)
+ * (softmax - onehot(y)) in cfg->dtype (bf16: rounded to nearest even, like every
+ * other matrix-multiply operand), then dh = G W^T and dW = h^T G with fp32
+ * accumulation. Same conventions as the layer calls (device pointers owned by the
+ * caller, 16-byte alignment, asynchronous on `stream`, validation before launch).
+ */
+typedef struct {
+  int64_t T, D, V;       /* tokens, hidden width, vocabulary size                          */
+  int64_t ldw;           /* columns of W as stored: >= V and a multiple of 64. Columns       */
+                         /* V..ldw-1 are not logits, but must hold finite values (the        */
+                         /* backward multiplies them by zero)                                */
+  int64_t block_rows;    /* tokens whose logits are live at once; 0 = automatic (8192)       */
+  int32_t dtype;         /* bpt_dtype of h, W and dh                                          */
+  int32_t reserved;      /* must be 0                                                         */
+} bpt_xent_config;
+
+/* Host-only checks; D and ldw must be multiples of 64 (else BPT_ERR_UNSUPPORTED). */
+bpt_status bpt_xent_validate(const bpt_xent_config* cfg);
+
+/* Workspace of bpt_xent_fwd (backward = 0): block_rows * ldw fp32 logits + T floats;
+ * of bpt_xent_bwd (backward = 1): block_rows (rounded up to 64) * ldw elements of
+ * cfg->dtype. Returns 0 for an invalid configuration. Host-only. */
+size_t bpt_xent_workspace_bytes(const bpt_xent_config* cfg, int backward);
+
+/* Forward. targets: [T] int32 class indices; a target outside [0, V) makes that
+ * token's loss, and so *loss, NaN. Writes loss (one float) and lse [T] (fp32, the
+ * natural-log log-sum-exp of each token's logits, which the backward takes). */
+bpt_status bpt_xent_fwd(const bpt_xent_config* cfg, const void* h, const void* W, const int32_t* targets,
+                        float* loss, float* lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward for an upstream gradient dloss of the loss (host scalar). Writes dh [T, D]
+ * in cfg->dtype and, unless dW is NULL, dW [D, ldw] fp32 (columns from V on get 0).
+ * Both are OVERWRITTEN. A target outside [0, V) contributes no one-hot term. */
+bpt_status bpt_xent_bwd(const bpt_xent_config* cfg, const void* h, const void* W, const int32_t* targets,
+                        const float* lse, float dloss, void* dh, float* dW, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

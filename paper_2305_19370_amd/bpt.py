@@ -47,9 +47,15 @@ class SavedLayout(ctypes.Structure):
     _fields_ = [(n, c_sz) for n in SAVED_FIELDS]
 
 
+class XentConfig(ctypes.Structure):
+    _fields_ = [("T", c_i64), ("D", c_i64), ("V", c_i64), ("ldw", c_i64), ("block_rows", c_i64),
+                ("dtype", c_i32), ("reserved", c_i32)]
+
+
 EXPORTS = ("bpt_validate", "bpt_group_rows", "bpt_saved_bytes", "bpt_saved_layout_of", "bpt_workspace_bytes",
            "bpt_layer_fwd", "bpt_layer_bwd", "bpt_status_string", "bpt_last_error", "bpt_describe",
-           "bpt_profile_enable", "bpt_profile_report")
+           "bpt_profile_enable", "bpt_profile_report", "bpt_xent_validate", "bpt_xent_workspace_bytes",
+           "bpt_xent_fwd", "bpt_xent_bwd")
 
 _lib = None
 
@@ -88,6 +94,14 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.bpt_profile_enable.restype = c_i32
     lib.bpt_profile_report.argtypes = [ctypes.c_char_p, c_sz]
     lib.bpt_profile_report.restype = c_sz
+    lib.bpt_xent_validate.argtypes = [P(XentConfig)]
+    lib.bpt_xent_validate.restype = c_i32
+    lib.bpt_xent_workspace_bytes.argtypes = [P(XentConfig), c_i32]
+    lib.bpt_xent_workspace_bytes.restype = c_sz
+    lib.bpt_xent_fwd.argtypes = [P(XentConfig), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
+    lib.bpt_xent_fwd.restype = c_i32
+    lib.bpt_xent_bwd.argtypes = [P(XentConfig), c_vp, c_vp, c_vp, c_vp, c_f32, c_vp, c_vp, c_vp, c_sz, c_vp]
+    lib.bpt_xent_bwd.restype = c_i32
     _lib = lib
     return lib
 
@@ -247,3 +261,56 @@ class Layer:
             "mu2": view("mu2", T, torch.float32, (T,)),
             "rstd2": view("rstd2", T, torch.float32, (T,)),
         }
+
+
+# ---------------------------------------------------------------- cross-entropy of an LM head
+def make_xent_config(T: int, D: int, V: int, ldw: Optional[int] = None, block_rows: int = 0,
+                     dtype: str = "bf16") -> XentConfig:
+    dt = {"f32": BPT_F32, "bf16": BPT_BF16}
+    return XentConfig(T, D, V, ldw if ldw is not None else (V + 63) // 64 * 64, block_rows, dt[dtype], 0)
+
+
+def xent_validate(cfg: XentConfig) -> int:
+    return load().bpt_xent_validate(ctypes.byref(cfg))
+
+
+def xent_workspace_bytes(cfg: XentConfig, backward: bool) -> int:
+    return load().bpt_xent_workspace_bytes(ctypes.byref(cfg), int(backward))
+
+
+def xent_fwd(cfg: XentConfig, h: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, loss: torch.Tensor,
+             lse: torch.Tensor, workspace: torch.Tensor) -> None:
+    _check(load().bpt_xent_fwd(ctypes.byref(cfg), h.data_ptr(), W.data_ptr(), targets.data_ptr(),
+                               loss.data_ptr(), lse.data_ptr(), workspace.data_ptr(),
+                               workspace.numel() * workspace.element_size(), _stream()))
+
+
+def xent_bwd(cfg: XentConfig, h: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, lse: torch.Tensor,
+             dloss: float, dh: torch.Tensor, dW: Optional[torch.Tensor], workspace: torch.Tensor) -> None:
+    _check(load().bpt_xent_bwd(ctypes.byref(cfg), h.data_ptr(), W.data_ptr(), targets.data_ptr(),
+                               lse.data_ptr(), float(dloss), dh.data_ptr(), _ptr(dW), workspace.data_ptr(),
+                               workspace.numel() * workspace.element_size(), _stream()))
+
+
+class LMHeadLoss:
+    """Cross-entropy of an LM head through libbpt; allocates its buffers with torch."""
+
+    def __init__(self, cfg: XentConfig, device: str = "cuda"):
+        _check(xent_validate(cfg))
+        self.cfg, self.device = cfg, device
+
+    def _bytes(self, n: int) -> torch.Tensor:
+        return torch.empty(max(n, 256), dtype=torch.uint8, device=self.device)
+
+    def forward(self, h: torch.Tensor, W: torch.Tensor, targets: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor]:
+        loss = torch.empty(1, dtype=torch.float32, device=self.device)
+        lse = torch.empty(self.cfg.T, dtype=torch.float32, device=self.device)
+        xent_fwd(self.cfg, h, W, targets, loss, lse, self._bytes(xent_workspace_bytes(self.cfg, False)))
+        return loss, lse
+
+    def backward(self, h: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, lse: torch.Tensor,
+                 dloss: float = 1.0, want_dW: bool = True) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+        dh = torch.empty(h.shape, dtype=h.dtype, device=self.device)
+        dW = torch.empty((self.cfg.D, self.cfg.ldw), dtype=torch.float32, device=self.device) if want_dW else None
+        xent_bwd(self.cfg, h, W, targets, lse, dloss, dh, dW, self._bytes(xent_workspace_bytes(self.cfg, True)))
+        return dh, dW

@@ -31,6 +31,13 @@ BPT_DEV void c2_store4(const GemmArgs& a, int64_t idx, f32x4 v) {
   }
 }
 
+// EPI_XENT: d loss / d logit of column n for a row with log-sum-exp lse and target y
+BPT_DEV float xent_grad(const GemmArgs& a, int64_t n, float v, float lse, int y) {
+  if (n >= a.nvalid) return 0.0f;
+  const float p = __builtin_amdgcn_exp2f((v - lse) * 1.4426950408889634f);
+  return a.alpha * (n == y ? p - 1.0f : p);
+}
+
 template <int EPI, typename CT, typename RT>
 BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float v) {
   CT* C = (CT*)a.C + z * a.sC;
@@ -55,6 +62,8 @@ BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float
     if (a.bias) v += a.bias[a.bias_on_m ? m : n];
     C[idx] = from_f32<CT>(gelu_f(v));
     if (a.C2) c2_store(a, z * a.sC2 + m * a.ldc2 + n, gelu_grad_f(v));
+  } else if constexpr (EPI == EPI_XENT) {
+    C[idx] = from_f32<CT>(xent_grad(a, n, v, a.rowv[m], a.tgt[m]));
   } else {  // EPI_MUL
     const RT* R = (const RT*)a.R + z * a.sR;
     C[idx] = from_f32<CT>(v * to_f32<RT>(R[m * a.ldr + n]));
@@ -117,6 +126,11 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
       d[e] = gp;
     }
     if (a.C2) c2_store4(a, z * a.sC2 + m * a.ldc2 + n, d);
+  } else if constexpr (EPI == EPI_XENT) {
+    const float lse = a.rowv[m];
+    const int y = a.tgt[m];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = xent_grad(a, n + e, v[e], lse, y);
   } else {
     v *= V4<RT>::ld((const RT*)a.R + z * a.sR + m * a.ldr + n);
   }
@@ -126,9 +140,11 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
 // Four consecutive columns n..n+3 of row m inside the stored width, from pointers
 // already at (m, n): c into C, r into R (EPI_RESID / EPI_MUL; for an fp32 C that
 // accumulates, the values of C already loaded); c2 is the element index of (m, n) in
-// C2 (EPI_GELU); bn at bias[n]; bm = bias[m] for a per-row bias.
+// C2 (EPI_GELU); bn at bias[n]; bm = bias[m] for a per-row bias, or the row's
+// log-sum-exp for EPI_XENT, whose column is n and target y.
 template <int EPI, typename CT, typename RT>
-BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const float* bn, float bm, f32x4 v) {
+BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const float* bn, float bm, f32x4 v,
+                      int64_t n = 0, int y = 0) {
   if constexpr (EPI == EPI_STORE) {
     v *= a.alpha;
     if constexpr (sizeof(CT) == 4) {
@@ -151,6 +167,9 @@ BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const
       d[e] = gp;
     }
     if (a.C2) c2_store4(a, c2, d);
+  } else if constexpr (EPI == EPI_XENT) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = xent_grad(a, n + e, v[e], bm, y);
   } else {
     v *= V4<RT>::ld((const RT*)r);
   }
@@ -515,13 +534,18 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
       for (int it = 0; it < 32 / RSTEP; ++it) {
         const int row = r0 + RSTEP * it;
         const f32x4 v = *(const f32x4*)(strip + row * PITCHF + c0);
-        const float bm = (EPI == EPI_GELU && a.bias && a.bias_on_m) ? a.bias[mrow + row] : 0.0f;
+        float bm = (EPI == EPI_GELU && a.bias && a.bias_on_m) ? a.bias[mrow + row] : 0.0f;
+        int y = 0;
+        if constexpr (EPI == EPI_XENT) {
+          bm = a.rowv[mrow + row];
+          y = a.tgt[mrow + row];
+        }
         if constexpr (PRE)
           epi_vec4<EPI, CT, RT>(a, cb + (int64_t)RSTEP * it * a.ldc, &pre[i % PD][it], 0, bb, bm, v);
         else
           epi_vec4<EPI, CT, RT>(a, cb + (int64_t)RSTEP * it * a.ldc,
                                 rb + (int64_t)RSTEP * it * a.ldr * RS,
-                                c2b + (int64_t)RSTEP * it * a.ldc2, bb, bm, v);
+                                c2b + (int64_t)RSTEP * it * a.ldc2, bb, bm, v, ncol + c0, y);
       }
       if (do_pre && i + PD < Cfg::TM) preload(i + PD);
     } else {
@@ -653,6 +677,9 @@ hipError_t gemm(Dt ab, Epi epi, Dt ct, Dt rt, const GemmArgs& a, hipStream_t s) 
     case EPI_GELU:
       return ct == F32 ? launch_typed<EPI_GELU, float, float>(ab, a, s)
                        : launch_typed<EPI_GELU, bf16, float>(ab, a, s);
+    case EPI_XENT:
+      return ct == F32 ? launch_typed<EPI_XENT, float, float>(ab, a, s)
+                       : launch_typed<EPI_XENT, bf16, float>(ab, a, s);
     case EPI_MUL:
       if (rt == F16)
         return ct == F32 ? launch_typed<EPI_MUL, float, f16>(ab, a, s)

@@ -17,6 +17,9 @@ enum Epi {
   EPI_RESID = 1,   // C = acc + R[m, n] (+ bias[n])
   EPI_GELU = 2,    // z = acc (+ bias[n] or bias[m]); C = GELU(z); C2 = GELU'(z) if C2
   EPI_MUL = 3,     // C = acc * R[m, n]  (R fp32 or fp16)
+  EPI_XENT = 4,    // cross-entropy gradient of logits acc: for n < nvalid
+                   // C = alpha (exp(acc - rowv[m]) - [n == tgt[m]]), rowv the row's
+                   // log-sum-exp; C = 0 for nvalid <= n
 };
 
 struct GemmArgs {
@@ -33,7 +36,11 @@ struct GemmArgs {
   int64_t sA = 0, sB = 0, sC = 0, sR = 0, sC2 = 0;   // batch strides in elements
   int batch = 1;
   int accumulate = 0;          // fp32 C only: C += acc
-  float alpha = 1.0f;          // EPI_STORE: acc is multiplied by alpha before it is stored
+  float alpha = 1.0f;          // EPI_STORE: acc is multiplied by alpha before it is stored;
+                               // EPI_XENT: the gradient's scale
+  const float* rowv = nullptr; // EPI_XENT: per-row log-sum-exp (natural log), [M]
+  const int32_t* tgt = nullptr;// EPI_XENT: per-row target column, [M]
+  int64_t nvalid = 0;          // EPI_XENT: columns from nvalid on are not logits
   int bias_on_m = 0;           // EPI_GELU: bias indexed by row instead of column
   // Transposed operands (trans_b with any epilogue, trans_a with EPI_STORE or EPI_GELU,
   // both with EPI_STORE): trans_a means A is stored K-major, element
@@ -116,5 +123,15 @@ hipError_t row_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols,
 // both are 0 for the padding positions s >= S
 hipError_t attn_delta(Dt t, const void* dout, const void* o, int64_t ld, const float* lse, float* ndelta,
                       float* nlse2, int B, int64_t S, int64_t Sp, int H, int dh, hipStream_t s);
+
+// ---------------------------------------------------------------- cross-entropy of an LM head
+// Per row t of a block of fp32 logits z [rows, ld]: lse[t] over the first V columns and
+// the token loss lse[t] - z[t, tgt[t]] (NaN for a target outside [0, V)).
+hipError_t xent_rows(const float* z, int64_t ld, int64_t rows, int64_t V, const int32_t* tgt, float* lse,
+                     float* tok, hipStream_t s);
+// out[0] = mean of x[0..n), summed in a fixed order
+hipError_t mean_of(const float* x, int64_t n, float* out, hipStream_t s);
+// bytes (a multiple of 4) of zeros at p, by a kernel (no memset node in captured graphs)
+hipError_t fill_zero(void* p, int64_t bytes, hipStream_t s);
 
 }  // namespace bpt

@@ -228,6 +228,59 @@ double attn_pairs(int64_t q0, int64_t q1, int64_t S, int causal) {
   return 0.5 * ((double)q1 * (q1 + 1) - (double)q0 * (q0 + 1));
 }
 
+
+// ---------------------------------------------------------------- cross-entropy of an LM head
+constexpr int64_t kDefaultXentRows = 8192;     // tokens whose logits are live at once
+
+bpt_status xent_check(const bpt_xent_config* c) {
+  if (!c) return fail(BPT_ERR_INVALID_ARG, "config is NULL");
+  if (c->T < 1 || c->D < 1 || c->V < 1)
+    return fail(BPT_ERR_INVALID_ARG, "T, D, V must be >= 1 (got %lld %lld %lld)", (long long)c->T,
+                (long long)c->D, (long long)c->V);
+  if (c->ldw < c->V) return fail(BPT_ERR_INVALID_ARG, "ldw=%lld < V=%lld", (long long)c->ldw, (long long)c->V);
+  if (c->block_rows < 0) return fail(BPT_ERR_INVALID_ARG, "block_rows must be >= 0");
+  if (c->dtype != BPT_F32 && c->dtype != BPT_BF16) return fail(BPT_ERR_INVALID_ARG, "dtype must be BPT_F32 or BPT_BF16");
+  if (c->reserved != 0) return fail(BPT_ERR_INVALID_ARG, "reserved must be 0");
+  if (c->ldw % 64 != 0 || c->D % 64 != 0)
+    return fail(BPT_ERR_UNSUPPORTED, "ldw and D must be multiples of 64 (got %lld, %lld)", (long long)c->ldw,
+                (long long)c->D);
+  if (c->T > ((int64_t)1 << 31) - 1) return fail(BPT_ERR_UNSUPPORTED, "T too large");
+  return BPT_OK;
+}
+
+struct XentDims {
+  int64_t T, D, V, ldw, R, Rp;   // R: rows per block; Rp: R rounded up to 64
+  size_t E;
+};
+
+XentDims xent_dims(const bpt_xent_config& c) {
+  XentDims d;
+  d.T = c.T; d.D = c.D; d.V = c.V; d.ldw = c.ldw;
+  d.R = std::min(c.block_rows > 0 ? c.block_rows : kDefaultXentRows, c.T);
+  d.Rp = rup(d.R, 64);
+  d.E = esize(c.dtype);
+  return d;
+}
+
+struct XentWs {
+  float* logits;   // forward: [R, ldw] fp32
+  float* tok;      // forward: [T] token losses
+  void* g;         // backward: [Rp, ldw] in dtype, the logits' gradient of one block
+};
+
+XentWs xent_ws(const XentDims& d, void* base, int backward, int64_t* total) {
+  Bump bp(base);
+  XentWs w{};
+  if (backward) {
+    w.g = bp.take(d.Rp * d.ldw * (int64_t)d.E);
+  } else {
+    w.logits = (float*)bp.take(d.R * d.ldw * 4);
+    w.tok = (float*)bp.take(d.T * 4);
+  }
+  *total = rup(bp.off, kAlign);
+  return w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -594,6 +647,96 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     RUN("reduce.layernorm", 0, (double)T * D * (E_ + 4),
         layer_norm_param_grad(E, X, sv.mu1, sv.rstd1, w.dU, G.dln1_g ? G.dln1_g : w.scratch,
                               G.dln1_b ? G.dln1_b : w.scratch + D, w.partial, T, D, s));
+  return BPT_OK;
+}
+
+// ---------------------------------------------------------------- cross-entropy of an LM head
+bpt_status bpt_xent_validate(const bpt_xent_config* cfg) { return xent_check(cfg); }
+
+size_t bpt_xent_workspace_bytes(const bpt_xent_config* cfg, int backward) {
+  if (xent_check(cfg) != BPT_OK) return 0;
+  int64_t total;
+  xent_ws(xent_dims(*cfg), nullptr, backward, &total);
+  return (size_t)total;
+}
+
+bpt_status bpt_xent_fwd(const bpt_xent_config* cfg, const void* h, const void* W, const int32_t* targets,
+                        float* loss, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  bpt_status st = xent_check(cfg);
+  if (st != BPT_OK) return st;
+  const void* ptrs[] = {h, W, targets, loss, lse, ws};
+  for (const void* q : ptrs) {
+    if (!q) return fail(BPT_ERR_INVALID_ARG, "h, W, targets, loss, lse and workspace must not be NULL");
+    if (!aligned16(q)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", q);
+  }
+  const XentDims d = xent_dims(*cfg);
+  int64_t need;
+  XentWs w = xent_ws(d, ws, 0, &need);
+  if ((int64_t)ws_bytes < need)
+    return fail(BPT_ERR_WORKSPACE, "workspace %zu bytes < required %lld", ws_bytes, (long long)need);
+  hipStream_t s = (hipStream_t)stream;
+  const Dt E = cfg->dtype == BPT_BF16 ? BF16 : F32;
+  const int64_t E_ = (int64_t)d.E;
+  for (int64_t t0 = 0; t0 < d.T; t0 += d.R) {
+    const int64_t r = std::min(d.R, d.T - t0);
+    GemmArgs g;   // logits of the block: h W, W read as it is stored (B operand K-major)
+    g.A = (const char*)h + t0 * d.D * E_; g.lda = d.D;
+    g.B = W; g.ldb = d.ldw; g.trans_b = 1;
+    g.C = w.logits; g.ldc = d.ldw; g.M = r; g.N = d.ldw; g.K = d.D;
+    RUN("xent.logits", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
+    RUN("xent.rows", 0, (double)r * d.ldw * 4,
+        xent_rows(w.logits, d.ldw, r, d.V, targets + t0, lse + t0, w.tok + t0, s));
+  }
+  RUN("xent.mean", 0, (double)d.T * 4, mean_of(w.tok, d.T, loss, s));
+  return BPT_OK;
+}
+
+bpt_status bpt_xent_bwd(const bpt_xent_config* cfg, const void* h, const void* W, const int32_t* targets,
+                        const float* lse, float dloss, void* dh, float* dW, void* ws, size_t ws_bytes,
+                        void* stream) {
+  bpt_status st = xent_check(cfg);
+  if (st != BPT_OK) return st;
+  const void* ptrs[] = {h, W, targets, lse, dh, ws};
+  for (const void* q : ptrs) {
+    if (!q) return fail(BPT_ERR_INVALID_ARG, "h, W, targets, lse, dh and workspace must not be NULL");
+    if (!aligned16(q)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", q);
+  }
+  if (dW && !aligned16(dW)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", (void*)dW);
+  const XentDims d = xent_dims(*cfg);
+  int64_t need;
+  XentWs w = xent_ws(d, ws, 1, &need);
+  if ((int64_t)ws_bytes < need)
+    return fail(BPT_ERR_WORKSPACE, "workspace %zu bytes < required %lld", ws_bytes, (long long)need);
+  hipStream_t s = (hipStream_t)stream;
+  const Dt E = cfg->dtype == BPT_BF16 ? BF16 : F32;
+  const int64_t E_ = (int64_t)d.E;
+  for (int64_t t0 = 0; t0 < d.T; t0 += d.R) {
+    const int64_t r = std::min(d.R, d.T - t0), rk = rup(r, 32);
+    const char* hb = (const char*)h + t0 * d.D * E_;
+    {   // G = (dloss / T)(softmax - onehot) of the block's logits, recomputed
+      GemmArgs g;
+      g.A = hb; g.lda = d.D; g.B = W; g.ldb = d.ldw; g.trans_b = 1;
+      g.C = w.g; g.ldc = d.ldw; g.M = r; g.N = d.ldw; g.K = d.D;
+      g.alpha = dloss / (float)d.T; g.rowv = lse + t0; g.tgt = targets + t0; g.nvalid = d.V;
+      RUN("xent.grad_logits", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_XENT, E, F32, g, s));
+    }
+    if (rk > r)   // the product over tokens below reads rk rows of G: zero the pad rows
+      RUN("xent.fill", 0, (double)(rk - r) * d.ldw * E_,
+          fill_zero((char*)w.g + r * d.ldw * E_, (rk - r) * d.ldw * E_, s));
+    {   // dh = G W^T (W rows are contiguous along the vocabulary: the plain NT form)
+      GemmArgs g;
+      g.A = w.g; g.lda = d.ldw; g.B = W; g.ldb = d.ldw;
+      g.C = (char*)dh + t0 * d.D * E_; g.ldc = d.D; g.M = r; g.N = d.D; g.K = d.ldw;
+      RUN("xent.dh", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
+    }
+    if (dW) {   // dW = h^T G: h and G both read token-major (G is zero past row r)
+      GemmArgs g;
+      g.A = hb; g.lda = d.D; g.trans_a = 1; g.a_rows = r;
+      g.B = w.g; g.ldb = d.ldw; g.trans_b = 1; g.b_rows = rk;
+      g.C = dW; g.ldc = d.ldw; g.M = d.D; g.N = d.ldw; g.K = rk; g.accumulate = t0 > 0;
+      RUN("xent.dW", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
+    }
+  }
   return BPT_OK;
 }
 

@@ -380,6 +380,82 @@ __global__ __launch_bounds__(256) void copy2d_kernel(const T* in, int64_t ld_in,
 }
 
 // ------------------------------------------------------------------ host launchers
+
+// ------------------------------------------------------------------ cross-entropy rows
+// (m, l) summarises exp over a set of logits as l * exp(m); two summaries combine
+// exactly. m = -inf, l = 0 is the empty set.
+BPT_DEV void lse_merge(float& m, float& l, float m2, float l2) {
+  const float mm = fmaxf(m, m2);
+  if (mm == -__builtin_inff()) return;
+  l = l * __expf(m - mm) + l2 * __expf(m2 - mm);
+  m = mm;
+}
+
+// One workgroup per row t of a block of logits z (fp32, row stride ld, 16-byte aligned
+// rows): each thread summarises its columns of [0, V) online, the summaries combine by
+// shuffles and through LDS, and thread 0 writes lse[t] = m + log l and the token loss
+// lse[t] - z[t, y_t], or NaN when the target is outside [0, V).
+__global__ __launch_bounds__(256) void xent_rows_kernel(const float* z, int64_t ld, int64_t V,
+                                                        const int32_t* tgt, float* lse, float* tok) {
+  const int64_t t = blockIdx.x;
+  const float* zr = z + t * ld;
+  const int tid = threadIdx.x;
+  float m = -__builtin_inff(), l = 0.0f;
+  for (int64_t v = 4 * (int64_t)tid; v < V; v += 4 * 256) {
+    float x[4];
+    if (v + 4 <= V) {
+      const f32x4 q = *(const f32x4*)(zr + v);
+      x[0] = q[0]; x[1] = q[1]; x[2] = q[2]; x[3] = q[3];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[e] = v + e < V ? zr[v + e] : -__builtin_inff();
+    }
+    const float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    float s = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s += __expf(x[e] - mx);
+    lse_merge(m, l, mx, s);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, 64), l2 = __shfl_xor(l, o, 64);
+    lse_merge(m, l, m2, l2);
+  }
+  __shared__ float sm[4], sl[4];
+  if ((tid & 63) == 0) {
+    sm[tid >> 6] = m;
+    sl[tid >> 6] = l;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    m = sm[0];
+    l = sl[0];
+    for (int w = 1; w < 4; ++w) lse_merge(m, l, sm[w], sl[w]);
+    const float r = m + __logf(l);
+    lse[t] = r;
+    const int y = tgt[t];
+    tok[t] = (y >= 0 && y < V) ? r - zr[y] : __builtin_nanf("");
+  }
+}
+
+// out[0] = (sum of x[0..n)) / n, summed in a fixed order by one workgroup.
+__global__ __launch_bounds__(1024) void mean_kernel(const float* x, int64_t n, float* out) {
+  __shared__ float part[1024];
+  float s = 0.0f;
+  for (int64_t i = threadIdx.x; i < n; i += 1024) s += x[i];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 512; w >= 1; w >>= 1) {
+    if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = part[0] / (float)n;
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = 0u;
+}
+
 #define BPT_T(dt, T, ...) \
   do {                   \
     if ((dt) == F32) {   \
@@ -506,6 +582,29 @@ hipError_t copy2d(Dt t, const void* in, int64_t ld_in, void* out, int64_t ld_out
   const unsigned gx = (unsigned)((cols + 255) / 256 < 64 ? (cols + 255) / 256 : 64);
   BPT_T(t, T, hipLaunchKernelGGL((copy2d_kernel<T>), dim3(gx, (unsigned)rows), dim3(256), 0, s,
                                  (const T*)in, ld_in, (T*)out, ld_out, cols));
+  return hipGetLastError();
+}
+
+hipError_t xent_rows(const float* z, int64_t ld, int64_t rows, int64_t V, const int32_t* tgt, float* lse,
+                     float* tok, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (ld % 4 != 0 || ((uintptr_t)z & 15) != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(xent_rows_kernel, dim3((unsigned)rows), dim3(256), 0, s, z, ld, V, tgt, lse, tok);
+  return hipGetLastError();
+}
+
+hipError_t mean_of(const float* x, int64_t n, float* out, hipStream_t s) {
+  if (n <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(1024), 0, s, x, n, out);
+  return hipGetLastError();
+}
+
+hipError_t fill_zero(void* p, int64_t bytes, hipStream_t s) {
+  if (bytes <= 0) return hipSuccess;
+  if (bytes % 4 != 0) return hipErrorInvalidValue;
+  const int64_t n = bytes / 4;
+  const unsigned g = (unsigned)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(g), dim3(256), 0, s, (uint32_t*)p, n);
   return hipGetLastError();
 }
 
