@@ -116,6 +116,106 @@ def copy_probe(nbytes: int, reps: int) -> int:
     return 0
 
 
+XENT_SHAPE = dict(T=32768, D=4096, V=50257)     # 7B-shaped tokens and width, GPT-2 vocabulary
+
+
+def cpu_baseline_xent(D: int, V: int, ldw: int, sample_T: int):
+    """Time the float64 cross-entropy oracle (untuned) on sample_T tokens of the LM-head shape."""
+    import numpy as np
+    from bpt_inputs import make_xent_inputs
+    from oracle.xent import xent_bwd, xent_fwd
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([int(i.get("num_threads", 0)) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    inp = make_xent_inputs(sample_T, D, V, ldw, "bf16", seed=0)
+    h, W, y = inp["h"].double().numpy(), inp["W"].double().numpy(), inp["targets"].numpy()
+    t0 = time.perf_counter()
+    f = xent_fwd(h, W, y, V)
+    b = xent_bwd(h, W, y, V)
+    dt = time.perf_counter() - t0
+    assert np.isfinite(f["loss"]) and np.isfinite(b["dW"]).all()
+    fl = 6.0 * sample_T * D * V
+    return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"fwd+bwd of {sample_T} tokens of the same LM-head shape (D={D}, V={V}), "
+                      f"float64 numpy, {dt:.1f} s", "seconds": dt}
+
+
+def bench_xent(args) -> int:
+    """--xent: the blockwise LM-head cross-entropy (logits never stored whole), fwd+bwd."""
+    import torch
+    from bpt_inputs import make_xent_inputs
+    from paper_2305_19370_amd import bpt
+
+    T, D, V = XENT_SHAPE["T"], XENT_SHAPE["D"], XENT_SHAPE["V"]
+    ldw = (V + 63) // 64 * 64
+    torch.cuda.set_device(0)
+    print(f"[bench] xent T={T} D={D} V={V} ldw={ldw} bf16", file=sys.stderr, flush=True)
+    inp = make_xent_inputs(T, D, V, ldw, "bf16", seed=0)
+    h, W, y = inp["h"].cuda(), inp["W"].cuda(), inp["targets"].cuda()
+    del inp
+    cfg = bpt.make_xent_config(T, D, V, ldw, 0, "bf16")
+    wsf = torch.empty(bpt.xent_workspace_bytes(cfg, False), dtype=torch.uint8, device="cuda")
+    wsb = torch.empty(bpt.xent_workspace_bytes(cfg, True), dtype=torch.uint8, device="cuda")
+    loss = torch.empty(1, dtype=torch.float32, device="cuda")
+    lse = torch.empty(T, dtype=torch.float32, device="cuda")
+    dh = torch.empty_like(h)
+    dW = torch.empty((D, ldw), dtype=torch.float32, device="cuda")
+
+    def step():
+        bpt.xent_fwd(cfg, h, W, y, loss, lse, wsf)
+        bpt.xent_bwd(cfg, h, W, y, lse, 1.0, dh, dW, wsb)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    bpt.profile_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    bpt.profile_enable(False)
+    prof = bpt.profile_report()
+    ms = e0.elapsed_time(e1) / args.steps
+    ok = bool(torch.isfinite(loss).all() and torch.isfinite(dh.float()).all())
+    print(f"[bench] xent {args.steps} steps: {ms:.2f} ms/step, loss {loss.item():.4f}, finite={ok}",
+          file=sys.stderr, flush=True)
+    value = 6.0 * T * D * V / (ms / 1e3) / 1e12
+    name, rec = max(prof.items(), key=lambda kv: kv[1]["ms"])
+    achieved = rec["flops"] / (rec["ms"] / 1e3) / 1e12
+    out = {
+        "metric": "LM-head cross-entropy fwd+bwd TFLOP/s (blockwise over tokens, logits never stored whole)",
+        "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "lmhead_xent_t32768_d4096_v50257", "T": T, "D": D, "V": V, "ldw": ldw,
+                   "block_rows": min(8192, T)},
+        "pct_of_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
+        "tokens_per_s": round(T / (ms / 1e3), 1),
+        "peak_hbm_gib": round(torch.cuda.max_memory_allocated() / 2 ** 30, 3),
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_BF16_TFLOPS, "kernel": name,
+                     "launches_per_step": rec["count"] / args.steps, "avg_launch_ms": rec["ms"] / rec["count"],
+                     "traffic": None, "traffic_unit": "bytes per launch"},
+        "kernels": {k: {"ms_per_step": v["ms"] / args.steps,
+                        "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["flops"] > 0 and v["ms"] > 0 else None,
+                        "gbs": (v["bytes"] / (v["ms"] / 1e3) / 1e9) if v["ms"] > 0 else None}
+                    for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["ms"])},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle) on 256 tokens ...", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline_xent(D, V, ldw, 256)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    return 0 if ok else 1
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,6 +226,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES (counter calibration)")
+    ap.add_argument("--xent", action="store_true",
+                    help="measure the blockwise LM-head cross-entropy instead of the layer")
     args = ap.parse_args()
     if args.copy_probe:
         return copy_probe(args.copy_probe, 3)
@@ -133,6 +235,8 @@ def main() -> int:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
               "sharding of the layer is a design, not part of this build", file=sys.stderr)
         return 2
+    if args.xent:
+        return bench_xent(args)
 
     import torch
     from bpt_inputs import WORKLOADS, make_inputs
