@@ -65,3 +65,46 @@ def xent_bwd(h: np.ndarray, W: np.ndarray, targets: np.ndarray, V: int, g: float
         G = round_g(G)
     h64 = np.asarray(h, dtype=np.float64)
     return dict(dh=G @ np.asarray(W, dtype=np.float64)[:, :V].T, dW=h64.T @ G, G=G)
+
+
+# ---------------------------------------------------------------- restricted to rows / columns
+def xent_lse_rows(h: np.ndarray, W: np.ndarray, V: int, chunk: int = 1024) -> np.ndarray:
+    """lse of every token, computed chunk by chunk of tokens (each row is independent,
+    so this is the plain definition; it only bounds the memory of the logits)."""
+    out = np.empty(h.shape[0])
+    for t0 in range(0, h.shape[0], chunk):
+        z = xent_logits(h[t0:t0 + chunk], W, V)
+        m = z.max(axis=1)
+        out[t0:t0 + chunk] = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
+    return out
+
+
+def xent_dh_rows(h: np.ndarray, W: np.ndarray, targets: np.ndarray, V: int, rows: np.ndarray, T: int,
+                 g: float = 1.0, round_g=None) -> np.ndarray:
+    """dh of the selected tokens (T = all tokens, for the 1/T of the mean)."""
+    z = xent_logits(h[rows], W, V)
+    m = z.max(axis=1)
+    lse = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
+    G = np.exp(z - lse[:, None])
+    y = np.asarray(targets, dtype=np.int64)[rows]
+    ok = (y >= 0) & (y < V)
+    G[np.arange(len(rows))[ok], y[ok]] -= 1.0
+    G *= g / T
+    if round_g is not None:
+        G = round_g(G)
+    return G @ np.asarray(W, dtype=np.float64)[:, :V].T
+
+
+def xent_dW_cols(h: np.ndarray, W: np.ndarray, targets: np.ndarray, lse: np.ndarray, cols: np.ndarray,
+                 g: float = 1.0, round_g=None) -> np.ndarray:
+    """Columns `cols` of dW = h^T G, from the exact lse of every token."""
+    h64 = np.asarray(h, dtype=np.float64)
+    T = h64.shape[0]
+    z = h64 @ np.asarray(W, dtype=np.float64)[:, cols]            # [T, len(cols)]
+    G = np.exp(z - lse[:, None])
+    y = np.asarray(targets, dtype=np.int64)
+    G -= (y[:, None] == np.asarray(cols)[None, :])
+    G *= g / T
+    if round_g is not None:
+        G = round_g(G)
+    return h64.T @ G

@@ -96,3 +96,23 @@ def test_xent_bad_target_is_nan():
     assert math.isnan(f["loss"]) and math.isfinite(f["token_loss"][0])
     b = xent_bwd(h, W, np.array([0, -1]), 3)
     np.testing.assert_allclose(b["G"][1], np.full(3, 1.0 / 3.0) / 2.0, atol=1e-15)
+
+
+def test_xent_restricted_forms_match_the_full_definition():
+    from oracle.bf16_model import to_bf16
+    from oracle.xent import xent_dh_rows, xent_dW_cols, xent_lse_rows
+    rng = np.random.default_rng(4)
+    T, D, V = 37, 8, 23
+    h, W = rng.normal(size=(T, D)), rng.normal(size=(D, V + 9))
+    y = rng.integers(0, V, size=T)
+    f, b = xent_fwd(h, W, y, V), xent_bwd(h, W, y, V, g=0.3)
+    np.testing.assert_allclose(xent_lse_rows(h, W, V, chunk=5), f["lse"], atol=1e-13)
+    rows = np.array([0, 5, 36])
+    np.testing.assert_allclose(xent_dh_rows(h, W, y, V, rows, T, g=0.3), b["dh"][rows], atol=1e-13)
+    cols = np.array([0, 7, V - 1])
+    np.testing.assert_allclose(xent_dW_cols(h, W, y, f["lse"], cols, g=0.3), b["dW"][:, cols], atol=1e-13)
+    br = xent_bwd(h, W, y, V, g=0.3, round_g=to_bf16)
+    np.testing.assert_allclose(xent_dh_rows(h, W, y, V, rows, T, g=0.3, round_g=to_bf16), br["dh"][rows],
+                               atol=1e-13)
+    np.testing.assert_allclose(xent_dW_cols(h, W, y, f["lse"], cols, g=0.3, round_g=to_bf16),
+                               br["dW"][:, cols], atol=1e-13)
