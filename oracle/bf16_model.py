@@ -4,7 +4,7 @@
 float64, except that every tensor a bf16 matrix-core implementation must hand to
 a matrix multiply as an operand is rounded to bfloat16 (round to nearest even)
 first: the LayerNorm outputs, Q, K, V, the exp-weights before they multiply V,
-the attention output, the GELU output, and in the backward dO, dS, dZ, the
+the attention output, the FFN activation output, and in the backward dO, dS, dZ, the
 upstream gradient into the output projection and the Q/K/V gradients.
 Accumulations, softmax statistics and LayerNorm statistics stay in high
 precision, as the hardware's fp32 accumulators do.
@@ -23,7 +23,7 @@ from typing import Dict
 
 import numpy as np
 
-from .layer import LayerParams, gelu, gelu_grad, layer_norm_bwd, layer_norm_fwd
+from .layer import LayerParams, act_fwd, act_grad, layer_norm_bwd, layer_norm_fwd
 
 
 def to_bf16(x: np.ndarray) -> np.ndarray:
@@ -63,12 +63,12 @@ def bf16_layer_fwd_bwd(X: np.ndarray, p: LayerParams, H: int, causal: bool, dY: 
     Z = Vn @ p.W1
     if p.b1 is not None:
         Z = Z + p.b1
-    G = r(gelu(Z))
+    G = r(act_fwd(p, Z))
     Y = Hd + G @ p.W2
     if p.b2 is not None:
         Y = Y + p.b2
 
-    dZ = r((dY @ p.W2.T) * gelu_grad(Z))
+    dZ = r((dY @ p.W2.T) * act_grad(p, Z))
     out = dict(Y=Y, O=O, lse=lse, Hd=Hd)
     out["dW2"] = flat(G).T @ flat(dY)
     out["dW1"] = flat(Vn).T @ flat(dZ)

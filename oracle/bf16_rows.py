@@ -19,7 +19,7 @@ from typing import Dict
 import numpy as np
 
 from .bf16_model import to_bf16
-from .layer import LayerParams, gelu, gelu_grad, layer_norm_bwd, layer_norm_fwd
+from .layer import LayerParams, act_fwd, act_grad, layer_norm_bwd, layer_norm_fwd
 
 
 def bf16_rows_fwd_bwd(X: np.ndarray, p: LayerParams, H: int, causal: bool, rows: np.ndarray,
@@ -58,13 +58,13 @@ def bf16_rows_fwd_bwd(X: np.ndarray, p: LayerParams, H: int, causal: bool, rows:
     Z = Vn @ p.W1
     if p.b1 is not None:
         Z = Z + p.b1
-    G = r(gelu(Z))
+    G = r(act_fwd(p, Z))
     Y = Hd + G @ p.W2
     if p.b2 is not None:
         Y = Y + p.b2
 
     dY = dY_rows
-    dZ = r((dY @ p.W2.T) * gelu_grad(Z))
+    dZ = r((dY @ p.W2.T) * act_grad(p, Z))
     out = dict(Y=Y)
     out["dW2"] = flat(G).T @ flat(dY)
     out["dW1"] = flat(Vn).T @ flat(dZ)

@@ -23,7 +23,7 @@ import math
 
 import numpy as np
 
-from .layer import LayerParams, gelu, layer_norm_fwd
+from .layer import LayerParams, act_fwd, layer_norm_fwd
 
 
 def _attend_query_block(q_scaled, K, V, rows, causal, Bkv):
@@ -93,7 +93,7 @@ def blockwise_layer_fwd(X: np.ndarray, p: LayerParams, H: int, causal: bool, Bq:
             z = vn @ p.W1
             if p.b1 is not None:
                 z = z + p.b1
-            y = hd + gelu(z) @ p.W2
+            y = hd + act_fwd(p, z) @ p.W2
             if p.b2 is not None:
                 y = y + p.b2
             Y[b, q0:q1] = y

@@ -11,8 +11,9 @@ Section 4 "Model Configuration"):
     O  = concat_h softmax(Q_h K_h^T / sqrt(dh) + mask) V_h     (eq. 1)
     Hd = X + O Wo                    residual 1
     Vn = LN2(Hd)
-    Z  = Vn W1 + b1,  G = GELU(Z)    FFN first linear + activation (eq. 2,
-                                     exact-erf GELU in place of ReLU)
+    Z  = Vn W1 + b1,  G = act(Z)     FFN first linear + activation: eq. 2's
+                                     ReLU, or the exact-erf GELU of GPT models
+                                     (``LayerParams.activation``)
     Y  = Hd + G W2 + b2              FFN second linear + residual 2
 
 The paper's per-block output (Section 3) is the FFN of (attention + input)
@@ -52,6 +53,7 @@ class LayerParams:
     ln2_b: Optional[np.ndarray] = None
     b1: Optional[np.ndarray] = None
     b2: Optional[np.ndarray] = None
+    activation: str = "gelu"          # FFN activation: "gelu" or "relu" (eq. 2)
 
 
 PARAM_NAMES = ("ln1_g", "ln1_b", "Wq", "Wk", "Wv", "Wo", "ln2_g", "ln2_b", "W1", "b1", "W2", "b2")
@@ -65,9 +67,9 @@ def _f64(t) -> Optional[np.ndarray]:
     return t.detach().to("cpu").double().numpy()   # exact for bf16 / fp32 values
 
 
-def params_from_inputs(inputs: Dict) -> LayerParams:
+def params_from_inputs(inputs: Dict, activation: str = "gelu") -> LayerParams:
     """Build float64 parameters from a dict of tensors (exact upcast)."""
-    return LayerParams(**{k: _f64(inputs.get(k)) for k in PARAM_NAMES})
+    return LayerParams(**{k: _f64(inputs.get(k)) for k in PARAM_NAMES}, activation=activation)
 
 
 # --------------------------------------------------------------------------- LayerNorm
@@ -103,6 +105,24 @@ def gelu(z: np.ndarray) -> np.ndarray:
 def gelu_grad(z: np.ndarray) -> np.ndarray:
     """d/dz GELU(z) = Phi(z) + z * phi(z)."""
     return 0.5 * (1.0 + erf(z / SQRT2)) + z * INV_SQRT_2PI * np.exp(-0.5 * z * z)
+
+
+def relu(z: np.ndarray) -> np.ndarray:
+    """Eq. (2)'s max(0, z)."""
+    return np.maximum(z, 0.0)
+
+
+def relu_grad(z: np.ndarray) -> np.ndarray:
+    """d/dz max(0, z): 1 for z > 0, else 0 (the value 0 taken at z = 0)."""
+    return (z > 0).astype(np.float64)
+
+
+def act_fwd(p: "LayerParams", z: np.ndarray) -> np.ndarray:
+    return relu(z) if p.activation == "relu" else gelu(z)
+
+
+def act_grad(p: "LayerParams", z: np.ndarray) -> np.ndarray:
+    return relu_grad(z) if p.activation == "relu" else gelu_grad(z)
 
 
 # --------------------------------------------------------------------------- attention
@@ -152,7 +172,7 @@ def layer_fwd(X: np.ndarray, p: LayerParams, H: int, causal: bool, eps: float = 
     Z = Vn @ p.W1
     if p.b1 is not None:
         Z = Z + p.b1
-    G = gelu(Z)
+    G = act_fwd(p, Z)
     Y = Hd + G @ p.W2
     if p.b2 is not None:
         Y = Y + p.b2
@@ -176,7 +196,7 @@ def layer_bwd(cache: Dict, p: LayerParams, dY: np.ndarray) -> Dict[str, Optional
     dW2 = flat(cache["G"]).T @ flat(dY)
     db2 = dY.sum(axis=(0, 1)) if p.b2 is not None else None
     dG = dY @ p.W2.T
-    dZ = dG * gelu_grad(cache["Z"])
+    dZ = dG * act_grad(p, cache["Z"])
     db1 = dZ.sum(axis=(0, 1)) if p.b1 is not None else None
     dW1 = flat(cache["Vn"]).T @ flat(dZ)
     dVn = dZ @ p.W1.T

@@ -22,7 +22,7 @@ from typing import Dict, Optional
 
 import numpy as np
 
-from .layer import LayerParams, gelu, gelu_grad, layer_norm_bwd, layer_norm_fwd
+from .layer import LayerParams, act_fwd, act_grad, layer_norm_bwd, layer_norm_fwd
 
 
 def rows_layer_fwd_bwd(X: np.ndarray, p: LayerParams, H: int, causal: bool,
@@ -65,7 +65,7 @@ def rows_layer_fwd_bwd(X: np.ndarray, p: LayerParams, H: int, causal: bool,
     Z = Vn @ p.W1
     if p.b1 is not None:
         Z = Z + p.b1
-    G = gelu(Z)
+    G = act_fwd(p, Z)
     Y = Hd + G @ p.W2
     if p.b2 is not None:
         Y = Y + p.b2
@@ -75,7 +75,7 @@ def rows_layer_fwd_bwd(X: np.ndarray, p: LayerParams, H: int, causal: bool,
     dY = dY_rows
     flat = lambda a: a.reshape(-1, a.shape[-1])
     dW2 = flat(G).T @ flat(dY)
-    dZ = (dY @ p.W2.T) * gelu_grad(Z)
+    dZ = (dY @ p.W2.T) * act_grad(p, Z)
     dW1 = flat(Vn).T @ flat(dZ)
     dz2, dg2, dbeta2 = layer_norm_bwd(dZ @ p.W1.T, xhat2, rstd2, p.ln2_g)
     dHd = dY + dz2

@@ -140,7 +140,7 @@ def test_layer_bruteforce(causal):
     p = rand_params(rng, D, F)
     X = rng.normal(size=(B, S, D))
     Y, _ = layer_fwd(X, p, H, causal, EPS)
-    pl = {k: (None if v is None else v.tolist()) for k, v in vars(p).items()}
+    pl = {k: (None if v is None else v.tolist()) for k, v in vars(p).items() if k != "activation"}
     Yb = brute_layer(X.tolist(), pl, H, causal, EPS)
     np.testing.assert_allclose(Y, Yb, rtol=0, atol=1e-13)
 
@@ -274,11 +274,12 @@ GRAD_OF = {"dX": "X", "dWq": "Wq", "dWk": "Wk", "dWv": "Wv", "dWo": "Wo", "dW1":
            "dln2_b": "ln2_b"}
 
 
-@pytest.mark.parametrize("causal", [False, True])
-def test_finite_differences(causal):
+@pytest.mark.parametrize("causal,activation", [(False, "gelu"), (True, "gelu"), (True, "relu")])
+def test_finite_differences(causal, activation):
     rng = np.random.default_rng(11 + causal)
     B, S, D, H, F = 2, 7, 8, 2, 16
     p = rand_params(rng, D, F, scale=0.5)
+    p.activation = activation
     X = rng.normal(size=(B, S, D))
     dY = rng.normal(size=(B, S, D))
     Y, cache = layer_fwd(X, p, H, causal, EPS)
@@ -327,7 +328,8 @@ def torch_layer(X, p, H, causal, eps):
     import torch.nn.functional as Fn
     B, S, D = X.shape
     dh = D // H
-    t = {k: (None if v is None else torch.tensor(v, requires_grad=True)) for k, v in vars(p).items()}
+    t = {k: (None if v is None else torch.tensor(v, requires_grad=True)) for k, v in vars(p).items()
+         if k != "activation"}
     Xt = torch.tensor(X, requires_grad=True)
     U = Fn.layer_norm(Xt, (D,), t["ln1_g"], t["ln1_b"], eps)
     q = (U @ t["Wq"]).view(B, S, H, dh).transpose(1, 2)
@@ -341,7 +343,7 @@ def torch_layer(X, p, H, causal, eps):
     z = Fn.layer_norm(hd, (D,), t["ln2_g"], t["ln2_b"], eps) @ t["W1"]
     if t["b1"] is not None:
         z = z + t["b1"]
-    y = hd + Fn.gelu(z) @ t["W2"]
+    y = hd + (Fn.relu(z) if p.activation == "relu" else Fn.gelu(z)) @ t["W2"]
     if t["b2"] is not None:
         y = y + t["b2"]
     return y, Xt, t
@@ -349,10 +351,12 @@ def torch_layer(X, p, H, causal, eps):
 
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("affine,biases", [(True, True), (False, False)])
-def test_torch_autograd_crosscheck(causal, affine, biases):
+@pytest.mark.parametrize("activation", ["gelu", "relu"])
+def test_torch_autograd_crosscheck(causal, affine, biases, activation):
     rng = np.random.default_rng(13)
     B, S, D, H, F = 2, 37, 32, 4, 64
     p = rand_params(rng, D, F, affine=affine, biases=biases)
+    p.activation = activation
     X, dY = rng.normal(size=(B, S, D)), rng.normal(size=(B, S, D))
     Y, cache = layer_fwd(X, p, H, causal, EPS)
     g = layer_bwd(cache, p, dY)
@@ -457,3 +461,18 @@ def test_bf16_rows_model_without_rounding_is_the_rows_oracle(causal):
     np.testing.assert_allclose(m["Y"], Yr, rtol=0, atol=1e-12)
     for k in GRAD_OF:
         np.testing.assert_allclose(m[k], gr[k], rtol=0, atol=1e-11, err_msg=k)
+
+
+def test_relu_ffn_closed_form():
+    """With every FFN pre-activation positive (b1 large) eq. (2)'s ReLU FFN is the plain
+    affine map (Vn W1 + b1) W2 + b2; with every one negative it is b2 alone."""
+    rng = np.random.default_rng(17)
+    B, S, D, H, F = 1, 6, 8, 2, 12
+    X = rng.normal(size=(B, S, D))
+    for sign in (1.0, -1.0):
+        p = rand_params(rng, D, F)
+        p.activation = "relu"
+        p.b1 = sign * 1e3 * np.ones(F)
+        Y, c = layer_fwd(X, p, H, True, EPS)
+        lin = (c["Vn"] @ p.W1 + p.b1) @ p.W2 if sign > 0 else 0.0
+        np.testing.assert_allclose(Y, c["Hd"] + lin + p.b2, rtol=0, atol=1e-9)
