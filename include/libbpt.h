@@ -8,7 +8,7 @@
  *     O  = softmax(Q_h K_h^T / sqrt(dh) + mask) V_h, per head (eq. 1), computed
  *          blockwise with running max / sum rescaling (Section 3, eq. 3)
  *     Hd = X + O Wo
- *     Y  = Hd + GELU(LN2(Hd) W1 + b1) W2 + b2                 (eq. 2, GELU for ReLU)
+ *     Y  = Hd + act(LN2(Hd) W1 + b1) W2 + b2                  (eq. 2; act = GELU or ReLU)
  *
  * and, per Algorithm 1, the FFN and both residuals are applied to each group of
  * query blocks right after that group's attention, before the next group
@@ -68,7 +68,12 @@ typedef struct {
   int32_t group_blocks;    /* query blocks per FFN group (rows of the [., F] intermediate   */
                            /* live at once = group_blocks * Bq); 0 = automatic              */
   float ln_eps;            /* LayerNorm epsilon (biased variance), e.g. 1e-5                */
+  int32_t activation;      /* bpt_activation of the FFN                                     */
 } bpt_config;
+
+/* FFN activation: the exact-erf GELU of GPT models (default) or eq. (2)'s ReLU,
+ * max(0, z), whose derivative is taken as 0 at z = 0. */
+typedef enum { BPT_GELU = 0, BPT_RELU = 1 } bpt_activation;
 
 typedef struct {           /* device pointers; see the conventions above                    */
   const float *ln1_g, *ln1_b;              /* [D] fp32 or NULL                               */

@@ -60,13 +60,3 @@ BPT_DEV void gelu_both(float z, float& g, float& gp) {
   g = z * phi_cdf;
   gp = fmaf(z * 0.39894228040143268f, e, phi_cdf);                       // + z exp(-z^2/2) / sqrt(2 pi)
 }
-BPT_DEV float gelu_f(float z) {
-  float g, gp;
-  gelu_both(z, g, gp);
-  return g;
-}
-BPT_DEV float gelu_grad_f(float z) {
-  float g, gp;
-  gelu_both(z, g, gp);
-  return gp;
-}

@@ -31,6 +31,16 @@ BPT_DEV void c2_store4(const GemmArgs& a, int64_t idx, f32x4 v) {
   }
 }
 
+// FFN activation of EPI_GELU and its derivative: GELU, or ReLU (derivative 0 at z = 0)
+BPT_DEV void act_both(const GemmArgs& a, float z, float& g, float& gp) {
+  if (a.relu) {
+    g = fmaxf(z, 0.0f);
+    gp = z > 0.0f ? 1.0f : 0.0f;
+  } else {
+    gelu_both(z, g, gp);
+  }
+}
+
 // EPI_XENT: d loss / d logit of column n for a row with log-sum-exp lse and target y
 BPT_DEV float xent_grad(const GemmArgs& a, int64_t n, float v, float lse, int y) {
   if (n >= a.nvalid) return 0.0f;
@@ -60,8 +70,10 @@ BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float
     C[idx] = from_f32<CT>(v);
   } else if constexpr (EPI == EPI_GELU) {
     if (a.bias) v += a.bias[a.bias_on_m ? m : n];
-    C[idx] = from_f32<CT>(gelu_f(v));
-    if (a.C2) c2_store(a, z * a.sC2 + m * a.ldc2 + n, gelu_grad_f(v));
+    float g, gp;
+    act_both(a, v, g, gp);
+    C[idx] = from_f32<CT>(g);
+    if (a.C2) c2_store(a, z * a.sC2 + m * a.ldc2 + n, gp);
   } else if constexpr (EPI == EPI_XENT) {
     C[idx] = from_f32<CT>(xent_grad(a, n, v, a.rowv[m], a.tgt[m]));
   } else {  // EPI_MUL
@@ -121,7 +133,7 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       float g, gp;
-      gelu_both(v[e], g, gp);
+      act_both(a, v[e], g, gp);
       v[e] = g;
       d[e] = gp;
     }
@@ -162,7 +174,7 @@ BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       float g, gp;
-      gelu_both(v[e], g, gp);
+      act_both(a, v[e], g, gp);
       v[e] = g;
       d[e] = gp;
     }

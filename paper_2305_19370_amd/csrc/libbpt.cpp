@@ -73,6 +73,8 @@ bpt_status check(const bpt_config* c) {
     return fail(BPT_ERR_INVALID_ARG, "dtype / out_dtype must be BPT_F32 or BPT_BF16");
   if (c->group_blocks < 0) return fail(BPT_ERR_INVALID_ARG, "group_blocks must be >= 0");
   if (!(c->ln_eps > 0.0f)) return fail(BPT_ERR_INVALID_ARG, "ln_eps must be > 0");
+  if (c->activation != BPT_GELU && c->activation != BPT_RELU)
+    return fail(BPT_ERR_INVALID_ARG, "activation must be BPT_GELU or BPT_RELU");
   const int64_t dh = c->D / c->H;
   if (dh != 64 && dh != 128)
     return fail(BPT_ERR_UNSUPPORTED, "head dim D/H=%lld unsupported (64 or 128)", (long long)dh);
@@ -349,13 +351,13 @@ size_t bpt_describe(const bpt_config* cfg, char* buf, size_t n) {
   const bool bf = cfg->dtype == BPT_BF16;
   int w = snprintf(buf, n,
                    "dtype=%s attention: q-tile=%d kv-step=%d (%s); backward dK/dV kv-tile=%d q-step=%d, "
-                   "dQ q-tile=%d kv-step=%d; gemm: %s; ffn group rows=%lld (%lld query blocks of %lld)",
+                   "dQ q-tile=%d kv-step=%d; gemm: %s; ffn %s, group rows=%lld (%lld query blocks of %lld)",
                    bf ? "bf16" : "f32", bf ? 256 : 64, bf ? 64 : 32,
                    bf ? "MFMA 32x32x16 bf16, fp32 accumulate, 32 rows per wave" : "fp32 VALU",
                    bf ? 256 : 64, bf ? 64 : 16, bf ? 256 : 64, bf ? 64 : 16,
                    bf ? "MFMA bf16 256x256 (8 waves) or 128x128 (4 waves) tiles, K-step 32"
                       : "fp32 VALU 64x64 tiles",
-                   (long long)d.R, (long long)((d.R + cfg->Bq - 1) / cfg->Bq), (long long)cfg->Bq);
+                   cfg->activation == BPT_RELU ? "relu" : "gelu", (long long)d.R, (long long)((d.R + cfg->Bq - 1) / cfg->Bq), (long long)cfg->Bq);
   return w < 0 ? 0 : std::min((size_t)w, n - 1);
 }
 
@@ -470,6 +472,7 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
       GemmArgs g1;     // G = GELU(LN2(h) W1 + b1)
       g1.A = w.vg; g1.lda = D; g1.B = p->W1; g1.ldb = F; g1.trans_b = 1; g1.C = w.gg; g1.ldc = F;
       g1.bias = p->b1; g1.M = r; g1.N = F; g1.K = D;
+      g1.relu = cfg->activation == BPT_RELU;
       RUN("gemm.ffn1", gemm_flops(g1), gemm_bytes(g1, E_, E_), gemm(E, EPI_GELU, E, F32, g1, s));
 
       GemmArgs g2;     // Y = h + G W2 + b2
@@ -534,6 +537,7 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
         g.A = p->W1; g.lda = F; g.trans_a = 1; g.B = w.vg; g.ldb = D;
         g.C = w.gT; g.ldc = d.Rp; g.C2 = w.gpT; g.ldc2 = d.Rp; g.c2t = GP;
         g.bias = p->b1; g.bias_on_m = 1; g.M = F; g.N = r; g.Nstore = rp; g.K = D;
+        g.relu = cfg->activation == BPT_RELU;
         RUN("gemm.bwd_ffn1_recompute", gemm_flops(g), gemm_bytes(g, E_, E_ + GP_), gemm(E, EPI_GELU, E, F32, g, s));
       }
       {   // dZ^T = (W2 dY^T) * GELU'(Z^T)

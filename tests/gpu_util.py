@@ -50,18 +50,18 @@ def run_gpu(w: Workload, inp: Dict, out_dtype: str = "f32", group_blocks: int = 
     return res
 
 
-def run_oracle(w: Workload, inp: Dict, backward: bool = True):
-    p = oracle.params_from_inputs(inp)
+def run_oracle(w: Workload, inp: Dict, backward: bool = True, activation: str = "gelu"):
+    p = oracle.params_from_inputs(inp, activation)
     X = inp["X"].double().numpy()
     Y, cache = oracle.layer_fwd(X, p, w.H, w.causal)
     g = oracle.layer_bwd(cache, p, inp["dY"].double().numpy()) if backward else None
     return Y, cache, g
 
 
-def bf16_model(w: Workload, inp: Dict) -> Dict:
+def bf16_model(w: Workload, inp: Dict, activation: str = "gelu") -> Dict:
     """The bf16-operand rounding model (oracle/bf16_model.py) on the same inputs."""
     from oracle.bf16_model import bf16_layer_fwd_bwd
-    p = oracle.params_from_inputs(inp)
+    p = oracle.params_from_inputs(inp, activation)
     return bf16_layer_fwd_bwd(inp["X"].double().numpy(), p, w.H, w.causal, inp["dY"].double().numpy())
 
 

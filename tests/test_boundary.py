@@ -163,3 +163,10 @@ def test_status_strings():
     assert lib.bpt_status_string(0) == b"BPT_OK"
     assert lib.bpt_status_string(3) == b"BPT_ERR_WORKSPACE"
     assert lib.bpt_status_string(99) == b"BPT_ERR_UNKNOWN"
+
+
+def test_activation_is_validated():
+    cfg = bpt.make_config(1, 256, 256, 2, 512, 64, 64, True, "bf16", activation="relu")
+    assert bpt.validate(cfg) == 0 and "relu" in bpt.describe(cfg)
+    cfg.activation = 7
+    assert bpt.validate(cfg) == 1

@@ -38,10 +38,10 @@ def bf16_limits(model_stats):
             max(BF16_E_MEAN, MODEL_FACTOR_MEAN * model_stats["e_mean"]))
 
 
-def compare_all(w, inp, gpu, Yr, g, tol_kind, label):
+def compare_all(w, inp, gpu, Yr, g, tol_kind, label, activation="gelu"):
     rows, bad = [], []
     names = ["Y", "dX"] + [n for n in GRAD_NAMES if n in gpu]
-    model = bf16_model(w, inp) if tol_kind == "bf16" else None
+    model = bf16_model(w, inp, activation) if tol_kind == "bf16" else None
     for n in names:
         ref = Yr if n == "Y" else g[n]
         s = stats(gpu[n].numpy(), ref)
@@ -88,6 +88,18 @@ def test_bf16_small_ragged(causal, S, H):
     gpu = run_gpu(w, inp, group_blocks=2)
     Yr, _, g = run_oracle(w, inp)
     compare_all(w, inp, gpu, Yr, g, "bf16", w.name)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_relu_ffn_with_biases(dtype):
+    """Eq. (2)'s FFN as printed: ReLU with both biases (the GELU of GPT models is the
+    default activation)."""
+    w = small_workload(dtype, B=2, S=250, D=256, H=2, F=512, causal=True, Bq=64, Bkv=64)
+    inp = make_inputs(w, seed=8, affine=True, biases=True)
+    say(f"case relu {w.name}")
+    gpu = run_gpu(w, inp, group_blocks=2, activation="relu")
+    Yr, _, g = run_oracle(w, inp, activation="relu")
+    compare_all(w, inp, gpu, Yr, g, "fp32" if dtype == "f32" else "bf16", w.name + "_relu", activation="relu")
 
 
 @pytest.mark.parametrize("causal", [True, False])
