@@ -31,9 +31,12 @@ BPT_DEV void c2_store4(const GemmArgs& a, int64_t idx, f32x4 v) {
   }
 }
 
-// FFN activation of EPI_GELU and its derivative: GELU, or ReLU (derivative 0 at z = 0)
-BPT_DEV void act_both(const GemmArgs& a, float z, float& g, float& gp) {
-  if (a.relu) {
+// the FFN activation epilogues and their activation with its derivative: GELU, or
+// ReLU (derivative 0 at z = 0)
+template <int EPI> constexpr bool kAct = EPI == EPI_GELU || EPI == EPI_RELU;
+template <int EPI>
+BPT_DEV void act_both(float z, float& g, float& gp) {
+  if constexpr (EPI == EPI_RELU) {
     g = fmaxf(z, 0.0f);
     gp = z > 0.0f ? 1.0f : 0.0f;
   } else {
@@ -54,7 +57,7 @@ BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float
   const int64_t idx = m * a.ldc + n;
   if (n >= a.N) {                                   // zero padding columns
     C[idx] = from_f32<CT>(0.0f);
-    if (EPI == EPI_GELU && a.C2) c2_store(a, z * a.sC2 + m * a.ldc2 + n, 0.0f);
+    if (kAct<EPI> && a.C2) c2_store(a, z * a.sC2 + m * a.ldc2 + n, 0.0f);
     return;
   }
   if constexpr (EPI == EPI_STORE) {
@@ -68,10 +71,10 @@ BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float
     v += to_f32<RT>(R[m * a.ldr + n]);
     if (a.bias) v += a.bias[n];
     C[idx] = from_f32<CT>(v);
-  } else if constexpr (EPI == EPI_GELU) {
+  } else if constexpr (kAct<EPI>) {
     if (a.bias) v += a.bias[a.bias_on_m ? m : n];
     float g, gp;
-    act_both(a, v, g, gp);
+    act_both<EPI>(v, g, gp);
     C[idx] = from_f32<CT>(g);
     if (a.C2) c2_store(a, z * a.sC2 + m * a.ldc2 + n, gp);
   } else if constexpr (EPI == EPI_XENT) {
@@ -124,7 +127,7 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
   } else if constexpr (EPI == EPI_RESID) {
     v += V4<RT>::ld((const RT*)a.R + z * a.sR + m * a.ldr + n);
     if (a.bias) v += *(const f32x4*)(a.bias + n);
-  } else if constexpr (EPI == EPI_GELU) {
+  } else if constexpr (kAct<EPI>) {
     if (a.bias) {
       if (a.bias_on_m) v += a.bias[m];
       else v += *(const f32x4*)(a.bias + n);
@@ -133,7 +136,7 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       float g, gp;
-      act_both(a, v[e], g, gp);
+      act_both<EPI>(v[e], g, gp);
       v[e] = g;
       d[e] = gp;
     }
@@ -152,7 +155,7 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
 // Four consecutive columns n..n+3 of row m inside the stored width, from pointers
 // already at (m, n): c into C, r into R (EPI_RESID / EPI_MUL; for an fp32 C that
 // accumulates, the values of C already loaded); c2 is the element index of (m, n) in
-// C2 (EPI_GELU); bn at bias[n]; bm = bias[m] for a per-row bias, or the row's
+// C2 (EPI_GELU / EPI_RELU); bn at bias[n]; bm = bias[m] for a per-row bias, or the row's
 // log-sum-exp for EPI_XENT, whose column is n and target y.
 template <int EPI, typename CT, typename RT>
 BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const float* bn, float bm, f32x4 v,
@@ -165,7 +168,7 @@ BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const
   } else if constexpr (EPI == EPI_RESID) {
     v += V4<RT>::ld((const RT*)r);
     if (a.bias) v += *(const f32x4*)bn;
-  } else if constexpr (EPI == EPI_GELU) {
+  } else if constexpr (kAct<EPI>) {
     if (a.bias) {
       if (a.bias_on_m) v += bm;
       else v += *(const f32x4*)bn;
@@ -174,7 +177,7 @@ BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       float g, gp;
-      act_both(a, v[e], g, gp);
+      act_both<EPI>(v[e], g, gp);
       v[e] = g;
       d[e] = gp;
     }
@@ -541,12 +544,12 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
       const float* bb = a.bias ? a.bias + ncol + c0 : nullptr;
       constexpr int RS = (int)sizeof(RT);
       // the GELU epilogue is long: keep its loop rolled (instruction cache)
-      constexpr int UNR = EPI == EPI_GELU ? 4 : 32 / RSTEP;
+      constexpr int UNR = kAct<EPI> ? 4 : 32 / RSTEP;
 #pragma unroll UNR
       for (int it = 0; it < 32 / RSTEP; ++it) {
         const int row = r0 + RSTEP * it;
         const f32x4 v = *(const f32x4*)(strip + row * PITCHF + c0);
-        float bm = (EPI == EPI_GELU && a.bias && a.bias_on_m) ? a.bias[mrow + row] : 0.0f;
+        float bm = (kAct<EPI> && a.bias && a.bias_on_m) ? a.bias[mrow + row] : 0.0f;
         int y = 0;
         if constexpr (EPI == EPI_XENT) {
           bm = a.rowv[mrow + row];
@@ -661,7 +664,7 @@ static hipError_t launch_typed(Dt ab, const GemmArgs& a, hipStream_t s) {
         (a.trans_b && ((a.b_cols > 0 ? a.b_cols : a.N) % 8 || a.ldb % 8)))
       return hipErrorInvalidValue;
     // instantiated combinations: B transposed with every epilogue, A transposed with
-    // the plain store and the GELU epilogue, both with the plain store
+    // the plain store and the activation epilogues, both with the plain store
     if (a.trans_a && a.trans_b) {
       if constexpr (EPI == EPI_STORE)
         return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, true, kNWN>(a, s)
@@ -669,7 +672,7 @@ static hipError_t launch_typed(Dt ab, const GemmArgs& a, hipStream_t s) {
       return hipErrorInvalidValue;
     }
     if (a.trans_a) {
-      if constexpr (EPI == EPI_STORE || EPI == EPI_GELU)
+      if constexpr (EPI == EPI_STORE || kAct<EPI>)
         return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, false, kNWN>(a, s)
                           : launch_bf16<128, 128, EPI, CT, RT, true, false>(a, s);
       return hipErrorInvalidValue;
@@ -689,6 +692,9 @@ hipError_t gemm(Dt ab, Epi epi, Dt ct, Dt rt, const GemmArgs& a, hipStream_t s) 
     case EPI_GELU:
       return ct == F32 ? launch_typed<EPI_GELU, float, float>(ab, a, s)
                        : launch_typed<EPI_GELU, bf16, float>(ab, a, s);
+    case EPI_RELU:
+      return ct == F32 ? launch_typed<EPI_RELU, float, float>(ab, a, s)
+                       : launch_typed<EPI_RELU, bf16, float>(ab, a, s);
     case EPI_XENT:
       return ct == F32 ? launch_typed<EPI_XENT, float, float>(ab, a, s)
                        : launch_typed<EPI_XENT, bf16, float>(ab, a, s);

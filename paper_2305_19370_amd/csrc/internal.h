@@ -15,12 +15,12 @@ enum Dt { F32 = 0, BF16 = 1, F16 = 2 };
 enum Epi {
   EPI_STORE = 0,   // C = acc            (fp32 C may accumulate: C += acc)
   EPI_RESID = 1,   // C = acc + R[m, n] (+ bias[n])
-  EPI_GELU = 2,    // z = acc (+ bias[n] or bias[m]); C = act(z); C2 = act'(z) if C2, with
-                   // act = GELU, or ReLU when relu is set
+  EPI_GELU = 2,    // z = acc (+ bias[n] or bias[m]); C = GELU(z); C2 = GELU'(z) if C2
   EPI_MUL = 3,     // C = acc * R[m, n]  (R fp32 or fp16)
   EPI_XENT = 4,    // cross-entropy gradient of logits acc: for n < nvalid
                    // C = alpha (exp(acc - rowv[m]) - [n == tgt[m]]), rowv the row's
                    // log-sum-exp; C = 0 for nvalid <= n
+  EPI_RELU = 5,    // as EPI_GELU with max(0, z) and its derivative (0 at z = 0)
 };
 
 struct GemmArgs {
@@ -29,7 +29,7 @@ struct GemmArgs {
   void* C = nullptr;
   const void* R = nullptr;     // residual (EPI_RESID) or multiplier (EPI_MUL)
   const float* bias = nullptr;
-  void* C2 = nullptr;          // second output of EPI_GELU, element type c2t (F32 or F16)
+  void* C2 = nullptr;          // second output of EPI_GELU / EPI_RELU, element type c2t (F32 or F16)
   Dt c2t = F32;
   int64_t M = 0, N = 0, K = 0;
   int64_t Nstore = 0;          // columns [N, Nstore) of C (and C2) are written with 0
@@ -42,9 +42,8 @@ struct GemmArgs {
   const float* rowv = nullptr; // EPI_XENT: per-row log-sum-exp (natural log), [M]
   const int32_t* tgt = nullptr;// EPI_XENT: per-row target column, [M]
   int64_t nvalid = 0;          // EPI_XENT: columns from nvalid on are not logits
-  int bias_on_m = 0;           // EPI_GELU: bias indexed by row instead of column
-  int relu = 0;                // EPI_GELU: max(0, z) (derivative 0 at z = 0) instead of GELU
-  // Transposed operands (trans_b with any epilogue, trans_a with EPI_STORE or EPI_GELU,
+  int bias_on_m = 0;           // EPI_GELU / EPI_RELU: bias indexed by row instead of column
+  // Transposed operands (trans_b with any epilogue, trans_a with EPI_STORE, EPI_GELU or EPI_RELU,
   // both with EPI_STORE): trans_a means A is stored K-major, element
   // (m, k) at A[k * lda + m]; likewise trans_b for B (element (n, k) at B[k * ldb + n]).
   // For such an operand, x_rows is the number of k rows that may be read (rows from

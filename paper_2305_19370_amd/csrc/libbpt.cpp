@@ -416,6 +416,7 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
   for (const void* q : ptrs)
     if (q && !aligned16(q)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", q);
   const Dims d = dims_of(*cfg);
+  const Epi act = cfg->activation == BPT_RELU ? EPI_RELU : EPI_GELU;   // FFN epilogue of eq. (2)
   int64_t need, stotal;
   FwdWs w = fwd_ws(d, ws, &need);
   if ((int64_t)ws_bytes < need)
@@ -472,8 +473,7 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
       GemmArgs g1;     // G = GELU(LN2(h) W1 + b1)
       g1.A = w.vg; g1.lda = D; g1.B = p->W1; g1.ldb = F; g1.trans_b = 1; g1.C = w.gg; g1.ldc = F;
       g1.bias = p->b1; g1.M = r; g1.N = F; g1.K = D;
-      g1.relu = cfg->activation == BPT_RELU;
-      RUN("gemm.ffn1", gemm_flops(g1), gemm_bytes(g1, E_, E_), gemm(E, EPI_GELU, E, F32, g1, s));
+      RUN("gemm.ffn1", gemm_flops(g1), gemm_bytes(g1, E_, E_), gemm(E, act, E, F32, g1, s));
 
       GemmArgs g2;     // Y = h + G W2 + b2
       g2.A = w.gg; g2.lda = F; g2.B = p->W2; g2.ldb = D; g2.trans_b = 1; g2.C = off(Y, t0 * D * EO);
@@ -502,6 +502,7 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
   for (const void* q : ptrs)
     if (q && !aligned16(q)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", q);
   const Dims d = dims_of(*cfg);
+  const Epi act = cfg->activation == BPT_RELU ? EPI_RELU : EPI_GELU;   // FFN epilogue of eq. (2)
   int64_t need, stotal;
   BwdWs w = bwd_ws(d, ws, &need);
   if ((int64_t)ws_bytes < need)
@@ -537,8 +538,7 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
         g.A = p->W1; g.lda = F; g.trans_a = 1; g.B = w.vg; g.ldb = D;
         g.C = w.gT; g.ldc = d.Rp; g.C2 = w.gpT; g.ldc2 = d.Rp; g.c2t = GP;
         g.bias = p->b1; g.bias_on_m = 1; g.M = F; g.N = r; g.Nstore = rp; g.K = D;
-        g.relu = cfg->activation == BPT_RELU;
-        RUN("gemm.bwd_ffn1_recompute", gemm_flops(g), gemm_bytes(g, E_, E_ + GP_), gemm(E, EPI_GELU, E, F32, g, s));
+        RUN("gemm.bwd_ffn1_recompute", gemm_flops(g), gemm_bytes(g, E_, E_ + GP_), gemm(E, act, E, F32, g, s));
       }
       {   // dZ^T = (W2 dY^T) * GELU'(Z^T)
         GemmArgs g;
