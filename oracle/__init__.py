@@ -31,6 +31,9 @@ Contents
                the blockwise scheme applies to the final loss): the plain,
                unblocked logits h W, log-sum-exp, mean token loss and its
                gradients dh, dW.
+``gpt``        A GPT training step (the models of Section 5): token and
+               position embedding, L layers of ``layer``, final LayerNorm,
+               the ``xent`` head, and an AdamW update.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against brute-force
 loops, closed forms, invariants, finite differences and an independent
