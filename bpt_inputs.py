@@ -146,3 +146,39 @@ def make_xent_inputs(T: int, D: int, V: int, ldw: int, dtype: str = "bf16", seed
     W[:, :V] = torch.randn((D, V), generator=g, dtype=torch.float32) * (logit_std / D ** 0.5)
     targets = torch.randint(0, V, (T,), generator=g, dtype=torch.int32)
     return {"h": h, "W": W.to(dt), "targets": targets}
+
+
+def make_gpt_inputs(L: int, B: int, S: int, D: int, F: int, V: int, ldw: int, dtype: str = "f32", seed: int = 0,
+                    pos_table: bool = True, biases: bool = True) -> Dict[str, torch.Tensor]:
+    """Parameters, tokens and targets of an L-layer GPT, CPU tensors keyed by parameter
+    name ("Wte", "Wpe", "Wout", "lnf_g", "lnf_b", "<l>.<name>" per layer, "tokens",
+    "targets"). One CPU generator, draws in the order Wte ~ N(0, 1) [V, D],
+    Wpe ~ N(0, 0.5^2) [S, D], Wout ~ N(0, 4/D) [D, V] (zero padding columns up to ldw),
+    then per layer Wq, Wk, Wv, Wo, W1, W2 ~ N(0, 1/D_in), ln1_g, ln2_g ~ 1 + N(0, 0.1^2),
+    ln1_b, ln2_b, b1, b2 ~ N(0, 0.1^2), then lnf_g ~ 1 + N(0, 0.1^2), lnf_b ~ N(0, 0.1^2),
+    tokens and targets uniform over [0, V) as int32 [B*S]. Matrices and tables are
+    rounded once to the dtype; vectors stay fp32."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    dt = torch_dtype(dtype)
+    rn = lambda *s: torch.randn(s, generator=g, dtype=torch.float32)
+    out: Dict[str, torch.Tensor] = {"Wte": rn(V, D).to(dt)}
+    if pos_table:
+        out["Wpe"] = (rn(S, D) * 0.5).to(dt)
+    Wout = torch.zeros((D, ldw), dtype=torch.float32)
+    Wout[:, :V] = rn(D, V) * (2.0 / D ** 0.5)
+    out["Wout"] = Wout.to(dt)
+    for l in range(L):
+        for name, (r, c) in (("Wq", (D, D)), ("Wk", (D, D)), ("Wv", (D, D)), ("Wo", (D, D)), ("W1", (D, F)),
+                             ("W2", (F, D))):
+            out[f"{l}.{name}"] = (rn(r, c) * r ** -0.5).to(dt)
+        for name, n in (("ln1_g", D), ("ln1_b", D), ("ln2_g", D), ("ln2_b", D), ("b1", F), ("b2", D)):
+            if name in ("b1", "b2") and not biases:
+                continue
+            t = rn(n) * 0.1
+            out[f"{l}.{name}"] = t + 1.0 if name.endswith("_g") else t
+    out["lnf_g"] = rn(D) * 0.1 + 1.0
+    out["lnf_b"] = rn(D) * 0.1
+    out["tokens"] = torch.randint(0, V, (B * S,), generator=g, dtype=torch.int32)
+    out["targets"] = torch.randint(0, V, (B * S,), generator=g, dtype=torch.int32)
+    return out

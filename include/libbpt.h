@@ -197,6 +197,76 @@ bpt_status bpt_xent_bwd(const bpt_xent_config* cfg, const void* h, const void* W
                         const float* lse, float dloss, void* dh, float* dW, void* workspace,
                         size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------ GPT training step
+ * Section 5 trains decoder-only GPT models (Table 1 shapes) made of the layer
+ * above. The entry points below are the rest of such a model's training step:
+ * the token and position embedding in front of the first layer, the final
+ * LayerNorm before the LM head (bpt_xent_*), and the AdamW update (Adam with
+ * decoupled weight decay; Section 5 trains with weight decay 0.1). Same
+ * conventions as above: device pointers, 16-byte aligned, asynchronous on
+ * `stream`, validated before any launch. */
+
+typedef struct {
+  int64_t B, S;          /* batch and sequence length: tokens [B, S], row t = b*S + s       */
+  int64_t D;             /* width, a multiple of 8                                           */
+  int64_t V;             /* vocabulary (rows of Wte)                                         */
+  int32_t dtype;         /* bpt_dtype of Wte, Wpe and X                                      */
+  int32_t grad_dtype;    /* bpt_dtype of the dX that bpt_embed_bwd reads                     */
+} bpt_embed_config;
+
+/* X[t] = Wte[tokens[t]] + Wpe[t mod S]. tokens: [B*S] int32; Wte [V, D]; Wpe [S, D]
+ * or NULL (no position table); X [B*S, D]. A token outside [0, V) gives a NaN row. */
+bpt_status bpt_embed_fwd(const bpt_embed_config* cfg, const int32_t* tokens, const void* Wte,
+                         const void* Wpe, void* X, void* stream);
+
+/* Gradients of the embedding for an upstream dX [B*S, D] (cfg->grad_dtype):
+ * dWte [V, D] fp32 = per vocabulary row, the sum of dX over the tokens equal to it
+ * (a token outside [0, V) adds nothing); dWpe [S, D] fp32 = sum over the batch.
+ * Both are OVERWRITTEN; NULL skips. dWte's rows are summed with floating-point
+ * atomics, so the order of the additions into a repeated token's row, and with it
+ * the last bits of that row, may differ between runs. */
+bpt_status bpt_embed_bwd(const bpt_embed_config* cfg, const int32_t* tokens, const void* dX, float* dWte,
+                         float* dWpe, void* stream);
+
+typedef struct {
+  int64_t rows, D;       /* rows of width D, D a multiple of 4                              */
+  float eps;             /* added to the biased variance                                    */
+  int32_t in_dtype;      /* bpt_dtype of X and dX                                           */
+  int32_t out_dtype;     /* bpt_dtype of Y and dY                                           */
+  int32_t reserved;      /* 0                                                               */
+} bpt_ln_config;
+
+/* Workspace of bpt_ln_bwd in bytes (the column-sum partials of dg, db and, for a
+ * bf16 dY, an fp32 copy of it). 0 for an invalid configuration. Host-only. */
+size_t bpt_ln_workspace_bytes(const bpt_ln_config* cfg);
+
+/* LayerNorm per row: Y = g (X - mean) rstd + b, rstd = 1/sqrt(var + eps), var the
+ * biased variance; the same LayerNorm as the layer's LN1/LN2. g, b: fp32 [D] or
+ * NULL (1, 0). mean, rstd: fp32 [rows], written for bpt_ln_bwd. */
+bpt_status bpt_ln_fwd(const bpt_ln_config* cfg, const void* X, const float* g, const float* b, void* Y,
+                      float* mean, float* rstd, void* stream);
+
+/* Backward of bpt_ln_fwd: dX [rows, D] (in_dtype) from dY (out_dtype), X and the
+ * saved mean/rstd; dg = sum_rows dY * xhat, db = sum_rows dY (fp32 [D], OVERWRITTEN;
+ * both NULL skips them, exactly one NULL is an error). */
+bpt_status bpt_ln_bwd(const bpt_ln_config* cfg, const void* X, const float* g, const float* mean,
+                      const float* rstd, const void* dY, void* dX, float* dg, float* db, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
+typedef struct {
+  float lr, beta1, beta2, eps, weight_decay;
+  int32_t lowp_dtype;    /* bpt_dtype of the rounded copy p_lowp                             */
+  int64_t step;          /* 1-based step count, for the bias corrections                    */
+} bpt_adamw_config;
+
+/* One AdamW step on n fp32 elements, in place:
+ *   m = beta1 m + (1 - beta1) g,   v = beta2 v + (1 - beta2) g^2,
+ *   p = p - lr wd p - lr (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps)
+ * and, unless p_lowp is NULL, p_lowp = p rounded to lowp_dtype (the copy the
+ * layer's kernels read). */
+bpt_status bpt_adamw_step(const bpt_adamw_config* cfg, int64_t n, float* p, const float* g, float* m, float* v,
+                          void* p_lowp, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -53,10 +53,25 @@ class XentConfig(ctypes.Structure):
                 ("dtype", c_i32), ("reserved", c_i32)]
 
 
+class EmbedConfig(ctypes.Structure):
+    _fields_ = [("B", c_i64), ("S", c_i64), ("D", c_i64), ("V", c_i64), ("dtype", c_i32), ("grad_dtype", c_i32)]
+
+
+class LnConfig(ctypes.Structure):
+    _fields_ = [("rows", c_i64), ("D", c_i64), ("eps", c_f32), ("in_dtype", c_i32), ("out_dtype", c_i32),
+                ("reserved", c_i32)]
+
+
+class AdamWConfig(ctypes.Structure):
+    _fields_ = [("lr", c_f32), ("beta1", c_f32), ("beta2", c_f32), ("eps", c_f32), ("weight_decay", c_f32),
+                ("lowp_dtype", c_i32), ("step", c_i64)]
+
+
 EXPORTS = ("bpt_validate", "bpt_group_rows", "bpt_saved_bytes", "bpt_saved_layout_of", "bpt_workspace_bytes",
            "bpt_layer_fwd", "bpt_layer_bwd", "bpt_status_string", "bpt_last_error", "bpt_describe",
            "bpt_profile_enable", "bpt_profile_report", "bpt_xent_validate", "bpt_xent_workspace_bytes",
-           "bpt_xent_fwd", "bpt_xent_bwd")
+           "bpt_xent_fwd", "bpt_xent_bwd", "bpt_embed_fwd", "bpt_embed_bwd", "bpt_ln_workspace_bytes",
+           "bpt_ln_fwd", "bpt_ln_bwd", "bpt_adamw_step")
 
 _lib = None
 
@@ -103,6 +118,18 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.bpt_xent_fwd.restype = c_i32
     lib.bpt_xent_bwd.argtypes = [P(XentConfig), c_vp, c_vp, c_vp, c_vp, c_f32, c_vp, c_vp, c_vp, c_sz, c_vp]
     lib.bpt_xent_bwd.restype = c_i32
+    lib.bpt_embed_fwd.argtypes = [P(EmbedConfig), c_vp, c_vp, c_vp, c_vp, c_vp]
+    lib.bpt_embed_fwd.restype = c_i32
+    lib.bpt_embed_bwd.argtypes = [P(EmbedConfig), c_vp, c_vp, c_vp, c_vp, c_vp]
+    lib.bpt_embed_bwd.restype = c_i32
+    lib.bpt_ln_workspace_bytes.argtypes = [P(LnConfig)]
+    lib.bpt_ln_workspace_bytes.restype = c_sz
+    lib.bpt_ln_fwd.argtypes = [P(LnConfig), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]
+    lib.bpt_ln_fwd.restype = c_i32
+    lib.bpt_ln_bwd.argtypes = [P(LnConfig), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
+    lib.bpt_ln_bwd.restype = c_i32
+    lib.bpt_adamw_step.argtypes = [P(AdamWConfig), c_i64, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]
+    lib.bpt_adamw_step.restype = c_i32
     _lib = lib
     return lib
 
@@ -316,3 +343,57 @@ class LMHeadLoss:
         dW = torch.empty((self.cfg.D, self.cfg.ldw), dtype=torch.float32, device=self.device) if want_dW else None
         xent_bwd(self.cfg, h, W, targets, lse, dloss, dh, dW, self._bytes(xent_workspace_bytes(self.cfg, True)))
         return dh, dW
+
+
+# ---------------------------------------------------------------- GPT training step pieces
+_DT = {"f32": BPT_F32, "bf16": BPT_BF16}
+
+
+def make_embed_config(B: int, S: int, D: int, V: int, dtype: str = "bf16", grad_dtype: Optional[str] = None):
+    return EmbedConfig(B, S, D, V, _DT[dtype], _DT[grad_dtype or dtype])
+
+
+def embed_fwd(cfg: EmbedConfig, tokens: torch.Tensor, Wte: torch.Tensor, Wpe: Optional[torch.Tensor],
+              X: torch.Tensor) -> None:
+    _check(load().bpt_embed_fwd(ctypes.byref(cfg), tokens.data_ptr(), Wte.data_ptr(), _ptr(Wpe), X.data_ptr(),
+                                _stream()))
+
+
+def embed_bwd(cfg: EmbedConfig, tokens: torch.Tensor, dX: torch.Tensor, dWte: Optional[torch.Tensor],
+              dWpe: Optional[torch.Tensor]) -> None:
+    _check(load().bpt_embed_bwd(ctypes.byref(cfg), tokens.data_ptr(), dX.data_ptr(), _ptr(dWte), _ptr(dWpe),
+                                _stream()))
+
+
+def make_ln_config(rows: int, D: int, eps: float = 1e-5, in_dtype: str = "bf16",
+                   out_dtype: Optional[str] = None) -> LnConfig:
+    return LnConfig(rows, D, eps, _DT[in_dtype], _DT[out_dtype or in_dtype], 0)
+
+
+def ln_workspace_bytes(cfg: LnConfig) -> int:
+    return load().bpt_ln_workspace_bytes(ctypes.byref(cfg))
+
+
+def ln_fwd(cfg: LnConfig, X: torch.Tensor, g: Optional[torch.Tensor], b: Optional[torch.Tensor], Y: torch.Tensor,
+           mean: torch.Tensor, rstd: torch.Tensor) -> None:
+    _check(load().bpt_ln_fwd(ctypes.byref(cfg), X.data_ptr(), _ptr(g), _ptr(b), Y.data_ptr(), mean.data_ptr(),
+                             rstd.data_ptr(), _stream()))
+
+
+def ln_bwd(cfg: LnConfig, X: torch.Tensor, g: Optional[torch.Tensor], mean: torch.Tensor, rstd: torch.Tensor,
+           dY: torch.Tensor, dX: torch.Tensor, dg: Optional[torch.Tensor], db: Optional[torch.Tensor],
+           workspace: torch.Tensor) -> None:
+    _check(load().bpt_ln_bwd(ctypes.byref(cfg), X.data_ptr(), _ptr(g), mean.data_ptr(), rstd.data_ptr(),
+                             dY.data_ptr(), dX.data_ptr(), _ptr(dg), _ptr(db), workspace.data_ptr(),
+                             workspace.numel() * workspace.element_size(), _stream()))
+
+
+def adamw_step(p: torch.Tensor, g: torch.Tensor, m: torch.Tensor, v: torch.Tensor, step: int, lr: float,
+               beta1: float = 0.9, beta2: float = 0.95, eps: float = 1e-8, weight_decay: float = 0.1,
+               p_lowp: Optional[torch.Tensor] = None) -> None:
+    """One AdamW update of the fp32 tensor p (in place, with its moments m, v); p_lowp,
+    if given, receives p rounded to its dtype."""
+    lowp = BPT_BF16 if p_lowp is not None and p_lowp.dtype == torch.bfloat16 else BPT_F32
+    cfg = AdamWConfig(lr, beta1, beta2, eps, weight_decay, lowp, step)
+    _check(load().bpt_adamw_step(ctypes.byref(cfg), p.numel(), p.data_ptr(), g.data_ptr(), m.data_ptr(),
+                                 v.data_ptr(), _ptr(p_lowp), _stream()))

@@ -92,7 +92,8 @@ hipError_t layer_norm(Dt ti, Dt to, const void* x, int64_t ldx, const float* g, 
                       void* out, int64_t ldo, float* mu, float* rstd, int64_t rows, int64_t D,
                       float eps, int use_stats, hipStream_t s);
 
-// out = resid + LN^T(dout), per row; out2 (optional, type t2) gets the same values.
+// out = resid + LN^T(dout), per row (resid may be null: 0); out2 (optional, type t2) gets
+// the same values.
 hipError_t layer_norm_bwd(Dt ti, const void* x, const float* mu, const float* rstd, const float* g,
                           const float* dout, Dt tr, const void* resid, Dt to, void* out,
                           Dt t2, void* out2, int64_t rows, int64_t D, hipStream_t s);
@@ -132,6 +133,21 @@ hipError_t xent_rows(const float* z, int64_t ld, int64_t rows, int64_t V, const 
                      float* tok, hipStream_t s);
 // out[0] = mean of x[0..n), summed in a fixed order
 hipError_t mean_of(const float* x, int64_t n, float* out, hipStream_t s);
+// ---------------------------------------------------------------- GPT step pieces
+// X[t] = Wte[tok[t]] + Wpe[t mod S] (Wpe may be null); NaN row for tok outside [0, V). D % 8 == 0.
+hipError_t embed_fwd(Dt t, const int32_t* tok, const void* Wte, const void* Wpe, void* X, int64_t rows,
+                     int64_t S, int64_t D, int64_t V, hipStream_t s);
+// dWte = 0, then dWte[tok[t]] += dX[t] (fp32 atomics)
+hipError_t embed_dwte(Dt t, const int32_t* tok, const void* dX, float* dWte, int64_t rows, int64_t D, int64_t V,
+                      hipStream_t s);
+// dWpe[s] = sum_b dX[b S + s] (overwrite)
+hipError_t embed_dwpe(Dt t, const void* dX, float* dWpe, int64_t B, int64_t S, int64_t D, hipStream_t s);
+// out[i] = in[i] (bf16 -> fp32), n % 8 == 0
+hipError_t bf16_to_f32(const void* in, float* out, int64_t n, hipStream_t s);
+// one AdamW step over n fp32 elements; pl (type tl) gets the updated p when not null
+hipError_t adamw(Dt tl, float* p, const float* g, float* m, float* v, void* pl, int64_t n, float lr, float b1,
+                 float b2, float eps, float wd, float c1, float c2, hipStream_t s);
+
 // bytes (a multiple of 4) of zeros at p, by a kernel (no memset node in captured graphs)
 hipError_t fill_zero(void* p, int64_t bytes, hipStream_t s);
 

@@ -744,4 +744,162 @@ bpt_status bpt_xent_bwd(const bpt_xent_config* cfg, const void* h, const void* W
   return BPT_OK;
 }
 
+// ---------------------------------------------------------------- GPT training step pieces
+static bpt_status dtype_ok(int32_t t, const char* what) {
+  if (t != BPT_F32 && t != BPT_BF16) return fail(BPT_ERR_INVALID_ARG, "%s %d is not a bpt_dtype", what, (int)t);
+  return BPT_OK;
+}
+static Dt dt_of(int32_t t) { return t == BPT_BF16 ? BF16 : F32; }
+
+static bpt_status embed_check(const bpt_embed_config* c) {
+  if (!c) return fail(BPT_ERR_INVALID_ARG, "NULL config");
+  if (c->B < 1 || c->S < 1 || c->D < 1 || c->V < 1)
+    return fail(BPT_ERR_INVALID_ARG, "B, S, D, V must be >= 1");
+  if (c->D % 8) return fail(BPT_ERR_UNSUPPORTED, "D = %lld is not a multiple of 8", (long long)c->D);
+  if (c->B * c->S > INT32_MAX / 4 || c->V > INT32_MAX)
+    return fail(BPT_ERR_UNSUPPORTED, "B*S or V too large");
+  bpt_status st = dtype_ok(c->dtype, "dtype");
+  return st != BPT_OK ? st : dtype_ok(c->grad_dtype, "grad_dtype");
+}
+
+bpt_status bpt_embed_fwd(const bpt_embed_config* cfg, const int32_t* tokens, const void* Wte, const void* Wpe,
+                         void* X, void* stream) {
+  bpt_status st = embed_check(cfg);
+  if (st != BPT_OK) return st;
+  if (!tokens || !Wte || !X) return fail(BPT_ERR_INVALID_ARG, "NULL tokens, Wte or X");
+  const void* ptrs[] = {tokens, Wte, Wpe, X};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", q);
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t T = cfg->B * cfg->S, E_ = cfg->dtype == BPT_BF16 ? 2 : 4;
+  RUN("gpt.embed", 0, (double)T * 4 + (double)T * cfg->D * E_ * (Wpe ? 3 : 2),
+      embed_fwd(dt_of(cfg->dtype), tokens, Wte, Wpe, X, T, cfg->S, cfg->D, cfg->V, s));
+  return BPT_OK;
+}
+
+bpt_status bpt_embed_bwd(const bpt_embed_config* cfg, const int32_t* tokens, const void* dX, float* dWte,
+                         float* dWpe, void* stream) {
+  bpt_status st = embed_check(cfg);
+  if (st != BPT_OK) return st;
+  if (!tokens || !dX) return fail(BPT_ERR_INVALID_ARG, "NULL tokens or dX");
+  const void* ptrs[] = {tokens, dX, dWte, dWpe};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", q);
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t T = cfg->B * cfg->S, G_ = cfg->grad_dtype == BPT_BF16 ? 2 : 4;
+  const Dt GT = dt_of(cfg->grad_dtype);
+  if (dWte)
+    RUN("gpt.embed_dWte", 0, (double)cfg->V * cfg->D * 4 + (double)T * cfg->D * (G_ + 4),
+        embed_dwte(GT, tokens, dX, dWte, T, cfg->D, cfg->V, s));
+  if (dWpe)
+    RUN("gpt.embed_dWpe", 0, (double)T * cfg->D * G_ + (double)cfg->S * cfg->D * 4,
+        embed_dwpe(GT, dX, dWpe, cfg->B, cfg->S, cfg->D, s));
+  return BPT_OK;
+}
+
+static bpt_status ln_check(const bpt_ln_config* c) {
+  if (!c) return fail(BPT_ERR_INVALID_ARG, "NULL config");
+  if (c->rows < 1 || c->D < 1) return fail(BPT_ERR_INVALID_ARG, "rows and D must be >= 1");
+  if (c->D % 8) return fail(BPT_ERR_UNSUPPORTED, "D = %lld is not a multiple of 8", (long long)c->D);
+  if (!(c->eps >= 0.0f)) return fail(BPT_ERR_INVALID_ARG, "eps must be >= 0");
+  if (c->rows > INT32_MAX) return fail(BPT_ERR_UNSUPPORTED, "rows too large");
+  bpt_status st = dtype_ok(c->in_dtype, "in_dtype");
+  return st != BPT_OK ? st : dtype_ok(c->out_dtype, "out_dtype");
+}
+
+// workspace of bpt_ln_bwd: column-sum partials, then (bf16 dY) an fp32 copy of dY
+static int64_t ln_ws_parts(const bpt_ln_config& c, int64_t* dy_off) {
+  const int64_t part = rup((int64_t)layer_norm_param_grad_ws(c.D) * 4, kAlign);
+  *dy_off = part;
+  return part + (c.out_dtype == BPT_BF16 ? rup(c.rows * c.D * 4, kAlign) : 0);
+}
+
+size_t bpt_ln_workspace_bytes(const bpt_ln_config* cfg) {
+  if (ln_check(cfg) != BPT_OK) return 0;
+  int64_t o;
+  return (size_t)ln_ws_parts(*cfg, &o);
+}
+
+bpt_status bpt_ln_fwd(const bpt_ln_config* cfg, const void* X, const float* g, const float* b, void* Y,
+                      float* mean, float* rstd, void* stream) {
+  bpt_status st = ln_check(cfg);
+  if (st != BPT_OK) return st;
+  if (!X || !Y || !mean || !rstd) return fail(BPT_ERR_INVALID_ARG, "NULL X, Y, mean or rstd");
+  if (X == Y) return fail(BPT_ERR_INVALID_ARG, "Y must not alias X");
+  const void* ptrs[] = {X, g, b, Y, mean, rstd};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", q);
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t R = cfg->rows, D = cfg->D;
+  const double io = (double)R * D * ((cfg->in_dtype == BPT_BF16 ? 2 : 4) + (cfg->out_dtype == BPT_BF16 ? 2 : 4));
+  RUN("gpt.ln_f", 0, io + (double)R * 8,
+      layer_norm(dt_of(cfg->in_dtype), dt_of(cfg->out_dtype), X, D, g, b, Y, D, mean, rstd, R, D, cfg->eps, 0, s));
+  return BPT_OK;
+}
+
+bpt_status bpt_ln_bwd(const bpt_ln_config* cfg, const void* X, const float* g, const float* mean,
+                      const float* rstd, const void* dY, void* dX, float* dg, float* db, void* ws,
+                      size_t ws_bytes, void* stream) {
+  bpt_status st = ln_check(cfg);
+  if (st != BPT_OK) return st;
+  if (!X || !mean || !rstd || !dY || !dX || !ws)
+    return fail(BPT_ERR_INVALID_ARG, "NULL X, mean, rstd, dY, dX or workspace");
+  if (dX == dY || dX == X) return fail(BPT_ERR_INVALID_ARG, "dX must not alias dY or X");
+  if ((dg == nullptr) != (db == nullptr))
+    return fail(BPT_ERR_INVALID_ARG, "dg and db must both be given or both be NULL");
+  const void* ptrs[] = {X, g, mean, rstd, dY, dX, dg, db, ws};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", q);
+  int64_t dy_off;
+  const int64_t need = ln_ws_parts(*cfg, &dy_off);
+  if ((int64_t)ws_bytes < need)
+    return fail(BPT_ERR_WORKSPACE, "workspace %zu bytes < required %lld", ws_bytes, (long long)need);
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t R = cfg->rows, D = cfg->D;
+  const Dt TI = dt_of(cfg->in_dtype);
+  const int64_t I_ = cfg->in_dtype == BPT_BF16 ? 2 : 4;
+  float* partial = (float*)ws;
+  const float* dy32 = (const float*)dY;
+  if (cfg->out_dtype == BPT_BF16) {
+    float* c = (float*)off(ws, dy_off);
+    RUN("gpt.ln_f_dy32", 0, (double)R * D * 6, bf16_to_f32(dY, c, R * D, s));
+    dy32 = c;
+  }
+  RUN("gpt.ln_f_bwd", 0, (double)R * D * (2 * I_ + 4) + (double)R * 8,
+      layer_norm_bwd(TI, X, mean, rstd, g, dy32, F32, nullptr, TI, dX, TI, nullptr, R, D, s));
+  if (dg) {
+    RUN("gpt.ln_f_params", 0, (double)R * D * (I_ + 4),
+        layer_norm_param_grad(TI, X, mean, rstd, dy32, dg, db, partial, R, D, s));
+  }
+  return BPT_OK;
+}
+
+bpt_status bpt_adamw_step(const bpt_adamw_config* cfg, int64_t n, float* p, const float* g, float* m, float* v,
+                          void* p_lowp, void* stream) {
+  if (!cfg) return fail(BPT_ERR_INVALID_ARG, "NULL config");
+  if (n < 0) return fail(BPT_ERR_INVALID_ARG, "n must be >= 0");
+  if (cfg->step < 1) return fail(BPT_ERR_INVALID_ARG, "step must be >= 1");
+  if (!(cfg->beta1 >= 0.0f && cfg->beta1 < 1.0f && cfg->beta2 >= 0.0f && cfg->beta2 < 1.0f))
+    return fail(BPT_ERR_INVALID_ARG, "beta1 and beta2 must lie in [0, 1)");
+  if (!(cfg->eps > 0.0f) || !(cfg->lr >= 0.0f) || !(cfg->weight_decay >= 0.0f))
+    return fail(BPT_ERR_INVALID_ARG, "eps must be > 0, lr and weight_decay >= 0");
+  if (p_lowp) {
+    bpt_status st = dtype_ok(cfg->lowp_dtype, "lowp_dtype");
+    if (st != BPT_OK) return st;
+  }
+  if (n == 0) return BPT_OK;
+  if (!p || !g || !m || !v) return fail(BPT_ERR_INVALID_ARG, "NULL p, g, m or v");
+  const void* ptrs[] = {p, g, m, v, p_lowp};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return fail(BPT_ERR_INVALID_ARG, "pointer %p is not 16-byte aligned", q);
+  hipStream_t s = (hipStream_t)stream;
+  const double c1 = 1.0 / (1.0 - std::pow((double)cfg->beta1, (double)cfg->step));
+  const double c2 = 1.0 / (1.0 - std::pow((double)cfg->beta2, (double)cfg->step));
+  const int64_t L_ = p_lowp ? (cfg->lowp_dtype == BPT_BF16 ? 2 : 4) : 0;
+  RUN("gpt.adamw", 0, (double)n * (28 + L_),
+      adamw(dt_of(cfg->lowp_dtype), p, g, m, v, p_lowp, n, cfg->lr, cfg->beta1, cfg->beta2, cfg->eps,
+            cfg->weight_decay, (float)c1, (float)c2, s));
+  return BPT_OK;
+}
+
 }  // extern "C"

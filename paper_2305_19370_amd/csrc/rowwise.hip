@@ -199,8 +199,8 @@ __global__ __launch_bounds__(256) void ln_bwd_reg_kernel(const TI* x, const floa
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     const int d = 8 * (lane + 64 * c);
-    float rv[8];
-    Vec8<TR>::load(resid + row * D + d, rv);
+    float rv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (resid) Vec8<TR>::load(resid + row * D + d, rv);
 #pragma unroll
     for (int e = 0; e < 8; ++e) rv[e] += rs * (gd[c][e] - s1 - xh[c][e] * s2);
     Vec8<TO>::store(out + row * D + d, rv);
@@ -234,10 +234,10 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const TI* x, const float* m
   s1 = warp_sum(s1) / (float)D;
   s2 = warp_sum(s2) / (float)D;
   for (int64_t d = 4 * lane; d < D; d += 256) {
-    float xv[4], dv[4], rv[4];
+    float xv[4], dv[4], rv[4] = {0, 0, 0, 0};
     Vec4<TI>::load(xr + d, xv);
     Vec4<float>::load(dr + d, dv);
-    Vec4<TR>::load(resid + row * D + d, rv);
+    if (resid) Vec4<TR>::load(resid + row * D + d, rv);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const float gd = g ? dv[e] * g[d + e] : dv[e];

@@ -170,3 +170,37 @@ def test_activation_is_validated():
     assert bpt.validate(cfg) == 0 and "relu" in bpt.describe(cfg)
     cfg.activation = 7
     assert bpt.validate(cfg) == 1
+
+
+def test_gpt_step_entries_validate_before_launch():
+    """Embedding, final LayerNorm and AdamW reject bad configurations and pointers
+    on the host (fake, never-dereferenced addresses; nothing launches)."""
+    lib = bpt.load()
+    e = bpt.make_embed_config(2, 64, 256, 1000, dtype="bf16")
+    assert lib.bpt_embed_fwd(ctypes.byref(e), None, 4096, None, 8192, None) == 1          # NULL tokens
+    assert lib.bpt_embed_fwd(ctypes.byref(e), 4096, 4104, None, 8192, None) == 1          # misaligned Wte
+    bad = bpt.make_embed_config(2, 64, 252, 1000)                                           # D % 8
+    assert lib.bpt_embed_fwd(ctypes.byref(bad), 4096, 8192, None, 16384, None) == 2
+    bad = bpt.EmbedConfig(2, 64, 256, 1000, 7, 0)                                           # dtype
+    assert lib.bpt_embed_bwd(ctypes.byref(bad), 4096, 8192, 16384, None, None) == 1
+    assert lib.bpt_embed_bwd(ctypes.byref(e), 4096, None, 16384, None, None) == 1         # NULL dX
+
+    ln = bpt.make_ln_config(128, 256, 1e-5, in_dtype="bf16")
+    n = bpt.ln_workspace_bytes(ln)
+    assert n >= 2 * 256 * 4 + 128 * 256 * 4          # partials + fp32 copy of a bf16 dY
+    assert bpt.ln_workspace_bytes(bpt.make_ln_config(128, 256, 1e-5, in_dtype="f32")) < n
+    assert bpt.ln_workspace_bytes(bpt.make_ln_config(0, 256)) == 0
+    assert bpt.ln_workspace_bytes(bpt.LnConfig(128, 256, -1.0, 0, 0, 0)) == 0
+    assert lib.bpt_ln_fwd(ctypes.byref(ln), 4096, None, None, 4096, 8192, 12288, None) == 1   # Y aliases X
+    assert lib.bpt_ln_bwd(ctypes.byref(ln), 4096, None, 8192, 12288, 16384, 20480, 24576, None,
+                          1 << 20, n, None) == 1                                            # dg without db
+    assert lib.bpt_ln_bwd(ctypes.byref(ln), 4096, None, 8192, 12288, 16384, 20480, None, None,
+                          1 << 20, n - 1, None) == 3                                        # short workspace
+
+    a = bpt.AdamWConfig(1e-3, 0.9, 0.95, 1e-8, 0.1, 1, 1)
+    assert lib.bpt_adamw_step(ctypes.byref(a), 0, None, None, None, None, None, None) == 0    # empty: no-op
+    assert lib.bpt_adamw_step(ctypes.byref(a), 8, None, 4096, 8192, 12288, None, None) == 1   # NULL p
+    assert lib.bpt_adamw_step(ctypes.byref(a), 8, 4100, 4096, 8192, 12288, None, None) == 1   # misaligned
+    for bad in (bpt.AdamWConfig(1e-3, 1.0, 0.95, 1e-8, 0.1, 1, 1), bpt.AdamWConfig(1e-3, 0.9, 0.95, 0.0, 0.1, 1, 1),
+                bpt.AdamWConfig(1e-3, 0.9, 0.95, 1e-8, 0.1, 1, 0), bpt.AdamWConfig(-1.0, 0.9, 0.95, 1e-8, 0.1, 1, 1)):
+        assert lib.bpt_adamw_step(ctypes.byref(bad), 8, 4096, 8192, 12288, 16384, None, None) == 1
