@@ -216,6 +216,136 @@ def bench_xent(args) -> int:
     return 0 if ok else 1
 
 
+# GPT-XL (1B) of Table 1 / Table 4: 24 layers, width 2048, 16 heads of 128, FFN 4x,
+# GPT-2 vocabulary; one 16K-token sequence per step (Table 4's batch at that length)
+GPT_SHAPE = dict(L=24, B=1, S=16384, D=2048, H=16, F=8192, V=50257, Bq=1024, Bkv=1024)
+
+
+def gpt_flops_step(L, B, S, D, F, V, causal=True):
+    """Model FLOPs of one training step: 3x the forward of L layers plus the LM head."""
+    return 3 * (L * model_flops_fwd(B, S, D, F, causal) + 2 * B * S * D * V)
+
+
+def cpu_baseline_gpt(shape: dict, sample_L: int, sample_S: int):
+    """Time the float64 GPT oracle (untuned) forward and backward on sample_L layers of the
+    model's shape and a sample_S-token sequence, then express its FLOP rate as tokens/s of
+    the full model. The oracle's AdamW is left out of the timing: its float64 temporaries
+    over the 100M-entry head alone take half a minute, which would swamp the sample."""
+    import numpy as np
+    from bpt_inputs import make_gpt_inputs
+    from oracle.gpt import GPTParams, gpt_fwd_bwd
+    from oracle.layer import LayerParams
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([int(i.get("num_threads", 0)) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    D, F, V, H = shape["D"], shape["F"], shape["V"], shape["H"]
+    inp = make_gpt_inputs(sample_L, 1, sample_S, D, F, V, (V + 63) // 64 * 64, dtype="bf16", seed=0)
+    f = lambda k: inp[k].double().numpy()
+    mats, vecs = ("Wq", "Wk", "Wv", "Wo", "W1", "W2"), ("ln1_g", "ln1_b", "ln2_g", "ln2_b", "b1", "b2")
+    P = GPTParams(Wte=f("Wte"), Wpe=f("Wpe"), lnf_g=f("lnf_g"), lnf_b=f("lnf_b"), Wout=f("Wout")[:, :V],
+                  layers=[LayerParams(**{k: f(f"{l}.{k}") for k in mats + vecs}) for l in range(sample_L)])
+    tok = inp["tokens"].numpy().reshape(1, sample_S)
+    tgt = inp["targets"].numpy().reshape(1, sample_S)
+    del inp
+    t0 = time.perf_counter()
+    g = gpt_fwd_bwd(tok, tgt, P, H)
+    dt = time.perf_counter() - t0
+    assert np.isfinite(g["loss"])
+    fl = gpt_flops_step(sample_L, 1, sample_S, D, F, V)
+    full_per_token = gpt_flops_step(shape["L"], 1, shape["S"], D, F, V) / shape["S"]
+    return {"value": fl / dt / full_per_token, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"fwd+bwd (AdamW not timed) of {sample_L} of the {shape['L']} layers (D={D}, F={F}, H={H}) plus the "
+                      f"V={V} head on one {sample_S}-token sequence, float64 numpy, {dt:.1f} s; its FLOP rate "
+                      f"({fl / dt / 1e12:.3f} TFLOP/s) divided by the full model's FLOPs per token at "
+                      f"S={shape['S']}", "seconds": dt}
+
+
+def bench_gpt(args) -> int:
+    """--gpt: one GPT-XL training step (embedding, 24 BPT layers, final LN, blockwise
+    LM-head loss, backward, AdamW) on synthetic tokens."""
+    import torch
+    from paper_2305_19370_amd import bpt
+    from paper_2305_19370_amd.gpt import GPT, GPTShape, cosine_lr
+
+    shp = dict(GPT_SHAPE)
+    if args.gpt_seq:
+        shp["S"] = args.gpt_seq
+    s = GPTShape(**shp, dtype="bf16")
+    torch.cuda.set_device(0)
+    print(f"[bench] gpt {s}", file=sys.stderr, flush=True)
+    m = GPT(s, device="cuda", seed=0)
+    g = torch.Generator(device="cpu").manual_seed(0)
+    tok = torch.randint(0, s.V, (s.B * s.S,), generator=g, dtype=torch.int32).cuda()
+    tgt = torch.randint(0, s.V, (s.B * s.S,), generator=g, dtype=torch.int32).cuda()
+    total = args.warmup + args.steps
+    it = [0]
+
+    def step():
+        m.train_step(tok, tgt, cosine_lr(it[0], 2e-4, 0, total))
+        it[0] += 1
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    bpt.profile_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    bpt.profile_enable(False)
+    prof = bpt.profile_report()
+    ms = e0.elapsed_time(e1) / args.steps
+    loss = float(m.loss.item())
+    ok = bool(torch.isfinite(m.loss).all())
+    print(f"[bench] gpt {args.steps} steps: {ms:.2f} ms/step, loss {loss:.4f}, finite={ok}",
+          file=sys.stderr, flush=True)
+    T = s.B * s.S
+    fl = gpt_flops_step(s.L, s.B, s.S, s.D, s.F, s.V)
+    name, rec = max(prof.items(), key=lambda kv: kv[1]["ms"])
+    if rec["flops"] > 0:
+        achieved = rec["flops"] / (rec["ms"] / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_BF16_TFLOPS}
+    else:
+        achieved = rec["bytes"] / (rec["ms"] / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS}
+    workload = f"gpt_xl_1b_s{s.S}"
+    roof.update({"kernel": name, "launches_per_step": rec["count"] / args.steps,
+                 "avg_launch_ms": rec["ms"] / rec["count"], "traffic": recorded_traffic(name, workload),
+                 "traffic_unit": "bytes per launch"})
+    out = {
+        "metric": "GPT training tokens/s per device (Table 4 analog: GPT-XL 1B, synthetic tokens)",
+        "value": round(T / (ms / 1e3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": workload, "L": s.L, "B": s.B, "S": s.S, "D": s.D, "H": s.H, "F": s.F, "V": s.V,
+                   "Bq": s.Bq, "Bkv": s.Bkv, "params": s.n_params(), "optimizer": "AdamW(0.9, 0.95, wd 0.1)"},
+        "model_tflops": round(fl / (ms / 1e3) / 1e12, 2),
+        "pct_of_peak": round(100 * fl / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+        "loss": loss,
+        "peak_hbm_gib": round(torch.cuda.max_memory_allocated() / 2 ** 30, 3),
+        "roofline": roof,
+        "kernels": {k: {"ms_per_step": v["ms"] / args.steps,
+                        "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["flops"] > 0 and v["ms"] > 0 else None,
+                        "gbs": (v["bytes"] / (v["ms"] / 1e3) / 1e9) if v["ms"] > 0 else None}
+                    for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["ms"])},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle) on 4 layers x 2048 tokens ...", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline_gpt(shp, 4, 2048)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    return 0 if ok else 1
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -228,6 +358,9 @@ def main() -> int:
                     help="only run a plain device copy of BYTES (counter calibration)")
     ap.add_argument("--xent", action="store_true",
                     help="measure the blockwise LM-head cross-entropy instead of the layer")
+    ap.add_argument("--gpt", action="store_true",
+                    help="measure a GPT-XL (1B) training step (24 layers, head, AdamW) instead of the layer")
+    ap.add_argument("--gpt-seq", type=int, default=0, help="sequence length of --gpt (default 16384)")
     args = ap.parse_args()
     if args.copy_probe:
         return copy_probe(args.copy_probe, 3)
@@ -237,6 +370,8 @@ def main() -> int:
         return 2
     if args.xent:
         return bench_xent(args)
+    if args.gpt:
+        return bench_gpt(args)
 
     import torch
     from bpt_inputs import WORKLOADS, make_inputs

@@ -295,6 +295,78 @@ __global__ __launch_bounds__(256) void col_partial_kernel(const T* in, int64_t l
   partial[(int64_t)blockIdx.y * cols + c] = s;
 }
 
+// Wide forms of the two partial-sum kernels for 8-column-aligned rows: one wave per
+// (512-column group, row chunk), 8 consecutive columns per lane with 16-byte loads, rows
+// unrolled by four so that several loads are in flight per lane.
+template <typename T>
+__global__ __launch_bounds__(64) void col_partial8_kernel(const T* in, int64_t ld, int64_t rows, int64_t cols,
+                                                          float* partial) {
+  const int64_t c = ((int64_t)blockIdx.x * 64 + threadIdx.x) * 8;
+  if (c >= cols) return;
+  const int64_t per = (rows + kChunks - 1) / kChunks;
+  const int64_t r0 = blockIdx.y * per, r1 = r0 + per < rows ? r0 + per : rows;
+  float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  int64_t r = r0;
+  for (; r + 4 <= r1; r += 4) {
+    float v[4][8];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) Vec8<T>::load(in + (r + u) * ld + c, v[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[e] += v[u][e];
+  }
+  for (; r < r1; ++r) {
+    float v[8];
+    Vec8<T>::load(in + r * ld + c, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] += v[e];
+  }
+  Vec8<float>::store(partial + (int64_t)blockIdx.y * cols + c, s);
+}
+
+template <typename TI>
+__global__ __launch_bounds__(64) void ln_param_partial8_kernel(const TI* x, const float* mu, const float* rstd,
+                                                               const float* dout, float* partial, int64_t rows,
+                                                               int64_t D) {
+  const int64_t d = ((int64_t)blockIdx.x * 64 + threadIdx.x) * 8;
+  if (d >= D) return;
+  const int64_t per = (rows + kChunks - 1) / kChunks;
+  const int64_t r0 = blockIdx.y * per, r1 = r0 + per < rows ? r0 + per : rows;
+  float sg[8] = {0, 0, 0, 0, 0, 0, 0, 0}, sb[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  int64_t r = r0;
+  for (; r + 2 <= r1; r += 2) {
+    float xv[2][8], dv[2][8];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      Vec8<TI>::load(x + (r + u) * D + d, xv[u]);
+      Vec8<float>::load(dout + (r + u) * D + d, dv[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const float m = mu[r + u], rs = rstd[r + u];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        sg[e] = fmaf(dv[u][e], (xv[u][e] - m) * rs, sg[e]);
+        sb[e] += dv[u][e];
+      }
+    }
+  }
+  for (; r < r1; ++r) {
+    float xv[8], dv[8];
+    Vec8<TI>::load(x + r * D + d, xv);
+    Vec8<float>::load(dout + r * D + d, dv);
+    const float m = mu[r], rs = rstd[r];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      sg[e] = fmaf(dv[e], (xv[e] - m) * rs, sg[e]);
+      sb[e] += dv[e];
+    }
+  }
+  Vec8<float>::store(partial + (int64_t)blockIdx.y * D + d, sg);
+  Vec8<float>::store(partial + (int64_t)(kChunks + blockIdx.y) * D + d, sb);
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void row_sum_kernel(const T* in, int64_t ld, int64_t rows, int64_t cols,
                                                       float* out, int accumulate) {
@@ -526,9 +598,15 @@ size_t layer_norm_param_grad_ws(int64_t D) { return (size_t)2 * kChunks * (size_
 hipError_t layer_norm_param_grad(Dt ti, const void* x, const float* mu, const float* rstd,
                                  const float* dout, float* dgamma, float* dbeta, float* partial,
                                  int64_t rows, int64_t D, hipStream_t s) {
-  const dim3 grid((unsigned)((D + 255) / 256), kChunks);
-  BPT_T(ti, TI, hipLaunchKernelGGL((ln_param_partial_kernel<TI>), grid, dim3(256), 0, s, (const TI*)x,
-                                   mu, rstd, dout, partial, rows, D));
+  if (D % 8 == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)dout & 15) == 0 && ((uintptr_t)partial & 15) == 0) {
+    const dim3 grid8((unsigned)((D + 511) / 512), kChunks);
+    BPT_T(ti, TI, hipLaunchKernelGGL((ln_param_partial8_kernel<TI>), grid8, dim3(64), 0, s, (const TI*)x,
+                                     mu, rstd, dout, partial, rows, D));
+  } else {
+    const dim3 grid((unsigned)((D + 255) / 256), kChunks);
+    BPT_T(ti, TI, hipLaunchKernelGGL((ln_param_partial_kernel<TI>), grid, dim3(256), 0, s, (const TI*)x,
+                                     mu, rstd, dout, partial, rows, D));
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)((D + 255) / 256)), dim3(256), 0, s, partial,
@@ -538,9 +616,15 @@ hipError_t layer_norm_param_grad(Dt ti, const void* x, const float* mu, const fl
 
 hipError_t col_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols, float* out,
                    int accumulate, float* partial, hipStream_t s) {
-  const dim3 grid((unsigned)((cols + 255) / 256), kChunks);
-  BPT_T(t, T, hipLaunchKernelGGL((col_partial_kernel<T>), grid, dim3(256), 0, s, (const T*)in, ld, rows,
-                                 cols, partial));
+  if (cols % 8 == 0 && ld % 8 == 0 && ((uintptr_t)in & 15) == 0 && ((uintptr_t)partial & 15) == 0) {
+    const dim3 grid8((unsigned)((cols + 511) / 512), kChunks);
+    BPT_T(t, T, hipLaunchKernelGGL((col_partial8_kernel<T>), grid8, dim3(64), 0, s, (const T*)in, ld, rows,
+                                   cols, partial));
+  } else {
+    const dim3 grid((unsigned)((cols + 255) / 256), kChunks);
+    BPT_T(t, T, hipLaunchKernelGGL((col_partial_kernel<T>), grid, dim3(256), 0, s, (const T*)in, ld, rows,
+                                   cols, partial));
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)((cols + 255) / 256)), dim3(256), 0, s, partial,
