@@ -148,6 +148,8 @@ hipError_t bf16_to_f32(const void* in, float* out, int64_t n, hipStream_t s);
 hipError_t adamw(Dt tl, float* p, const float* g, float* m, float* v, void* pl, int64_t n, float lr, float b1,
                  float b2, float eps, float wd, float c1, float c2, hipStream_t s);
 
+// out[i] (+)= sum over z < nz of part[z n + i], added in slice order (n % 4 == 0)
+hipError_t sum_slices(const float* part, int nz, int64_t n, float* out, int accumulate, hipStream_t s);
 // bytes (a multiple of 4) of zeros at p, by a kernel (no memset node in captured graphs)
 hipError_t fill_zero(void* p, int64_t bytes, hipStream_t s);
 

@@ -683,6 +683,23 @@ hipError_t mean_of(const float* x, int64_t n, float* out, hipStream_t s) {
   return hipGetLastError();
 }
 
+__global__ __launch_bounds__(256) void sum_slices_kernel(const float* part, int nz, int64_t n, float* out,
+                                                         int accumulate) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;      // group of four
+  if (4 * q >= n) return;
+  f32x4 acc = accumulate ? ((const f32x4*)out)[q] : f32x4{0, 0, 0, 0};
+  for (int z = 0; z < nz; ++z) acc += ((const f32x4*)(part + z * n))[q];
+  ((f32x4*)out)[q] = acc;
+}
+
+hipError_t sum_slices(const float* part, int nz, int64_t n, float* out, int accumulate, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (n % 4 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(sum_slices_kernel, dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0, s, part, nz, n, out,
+                     accumulate);
+  return hipGetLastError();
+}
+
 hipError_t fill_zero(void* p, int64_t bytes, hipStream_t s) {
   if (bytes <= 0) return hipSuccess;
   if (bytes % 4 != 0) return hipErrorInvalidValue;
