@@ -31,6 +31,10 @@ Contents
                the blockwise scheme applies to the final loss): the plain,
                unblocked logits h W, log-sum-exp, mean token loss and its
                gradients dh, dW.
+``dropout``    Masks of the layer's two residual-branch dropouts (the mask the
+               paper's memory accounting keeps for the output projection and
+               for the FFN output), from Philox4x32-10 written from its
+               published definition; ``layer`` applies them when its rate > 0.
 ``gpt``        A GPT training step (the models of Section 5): token and
                position embedding, L layers of ``layer``, final LayerNorm,
                the ``xent`` head, and an AdamW update.

@@ -31,6 +31,8 @@ import math
 from typing import Dict, Optional
 
 import numpy as np
+
+from .dropout import dropout_factor
 from scipy.special import erf
 
 SQRT2 = math.sqrt(2.0)
@@ -54,6 +56,8 @@ class LayerParams:
     b1: Optional[np.ndarray] = None
     b2: Optional[np.ndarray] = None
     activation: str = "gelu"          # FFN activation: "gelu" or "relu" (eq. 2)
+    dropout: float = 0.0              # rate of the two residual-branch dropouts (0: none)
+    dropout_seed: int = 0             # 64-bit key of their masks (``oracle/dropout.py``)
 
 
 PARAM_NAMES = ("ln1_g", "ln1_b", "Wq", "Wk", "Wv", "Wo", "ln2_g", "ln2_b", "W1", "b1", "W2", "b2")
@@ -167,17 +171,21 @@ def layer_fwd(X: np.ndarray, p: LayerParams, H: int, causal: bool, eps: float = 
             cols = slice(h * dh, (h + 1) * dh)
             O[b, :, cols], _, lse[b, h] = attention_head(Q[b, :, cols], K[b, :, cols],
                                                          V[b, :, cols], causal)
-    Hd = X + O @ p.Wo
+    # dropout on the two residual branches (factor 1 where the rate is 0)
+    dm0 = dropout_factor(B * S, D, p.dropout_seed, 0, p.dropout).reshape(B, S, D)
+    dm1 = dropout_factor(B * S, D, p.dropout_seed, 1, p.dropout).reshape(B, S, D)
+    Hd = X + dm0 * (O @ p.Wo)
     Vn, xhat2, rstd2 = layer_norm_fwd(Hd, p.ln2_g, p.ln2_b, eps)
     Z = Vn @ p.W1
     if p.b1 is not None:
         Z = Z + p.b1
     G = act_fwd(p, Z)
-    Y = Hd + G @ p.W2
+    F2 = G @ p.W2
     if p.b2 is not None:
-        Y = Y + p.b2
+        F2 = F2 + p.b2
+    Y = Hd + dm1 * F2
     cache = dict(X=X, U=U, xhat1=xhat1, rstd1=rstd1, Q=Q, K=K, V=V, O=O, lse=lse, Hd=Hd,
-                 Vn=Vn, xhat2=xhat2, rstd2=rstd2, Z=Z, G=G, H=H, causal=causal)
+                 Vn=Vn, xhat2=xhat2, rstd2=rstd2, Z=Z, G=G, H=H, causal=causal, dm0=dm0, dm1=dm1)
     return Y, cache
 
 
@@ -192,10 +200,11 @@ def layer_bwd(cache: Dict, p: LayerParams, dY: np.ndarray) -> Dict[str, Optional
     dh = D // H
     flat = lambda a: a.reshape(-1, a.shape[-1])
 
-    # FFN and residual 2
-    dW2 = flat(cache["G"]).T @ flat(dY)
-    db2 = dY.sum(axis=(0, 1)) if p.b2 is not None else None
-    dG = dY @ p.W2.T
+    # FFN and residual 2 (the FFN branch sees dY through its dropout factor)
+    dF2 = cache["dm1"] * dY
+    dW2 = flat(cache["G"]).T @ flat(dF2)
+    db2 = dF2.sum(axis=(0, 1)) if p.b2 is not None else None
+    dG = dF2 @ p.W2.T
     dZ = dG * act_grad(p, cache["Z"])
     db1 = dZ.sum(axis=(0, 1)) if p.b1 is not None else None
     dW1 = flat(cache["Vn"]).T @ flat(dZ)
@@ -203,9 +212,10 @@ def layer_bwd(cache: Dict, p: LayerParams, dY: np.ndarray) -> Dict[str, Optional
     dz2, dg2, dbeta2 = layer_norm_bwd(dVn, cache["xhat2"], cache["rstd2"], p.ln2_g)
     dHd = dY + dz2
 
-    # output projection and attention
-    dWo = flat(O).T @ flat(dHd)
-    dO = dHd @ p.Wo.T
+    # output projection (through its dropout factor) and attention
+    dA = cache["dm0"] * dHd
+    dWo = flat(O).T @ flat(dA)
+    dO = dA @ p.Wo.T
     dQ, dK, dV = np.empty_like(Q), np.empty_like(K), np.empty_like(V)
     for b in range(B):
         for h in range(H):

@@ -140,7 +140,8 @@ def test_layer_bruteforce(causal):
     p = rand_params(rng, D, F)
     X = rng.normal(size=(B, S, D))
     Y, _ = layer_fwd(X, p, H, causal, EPS)
-    pl = {k: (None if v is None else v.tolist()) for k, v in vars(p).items() if k != "activation"}
+    pl = {k: (None if v is None else v.tolist()) for k, v in vars(p).items()
+          if k not in ("activation", "dropout", "dropout_seed")}
     Yb = brute_layer(X.tolist(), pl, H, causal, EPS)
     np.testing.assert_allclose(Y, Yb, rtol=0, atol=1e-13)
 
@@ -329,7 +330,7 @@ def torch_layer(X, p, H, causal, eps):
     B, S, D = X.shape
     dh = D // H
     t = {k: (None if v is None else torch.tensor(v, requires_grad=True)) for k, v in vars(p).items()
-         if k != "activation"}
+         if k not in ("activation", "dropout", "dropout_seed")}
     Xt = torch.tensor(X, requires_grad=True)
     U = Fn.layer_norm(Xt, (D,), t["ln1_g"], t["ln1_b"], eps)
     q = (U @ t["Wq"]).view(B, S, H, dh).transpose(1, 2)
