@@ -69,6 +69,13 @@ typedef struct {
                            /* live at once = group_blocks * Bq); 0 = automatic              */
   float ln_eps;            /* LayerNorm epsilon (biased variance), e.g. 1e-5                */
   int32_t activation;      /* bpt_activation of the FFN                                     */
+  float dropout;           /* rate p in [0, 1) of dropout on the two residual branches:     */
+                           /* h = X + drop(O Wo), Y = h + drop(FFN(LN2 h)); 0 = none        */
+  uint64_t dropout_seed;   /* key of the dropout masks: element (t, n) of branch k (0: O Wo,*/
+                           /* 1: FFN) uses word n%4 of Philox4x32-10 at counter             */
+                           /* (n/4, t, k, 0), t = b*S + s, key (seed low, seed high 32 bits);*/
+                           /* kept iff the word >= floor(p 2^32), kept values scaled by     */
+                           /* 1/(1 - p). Pass the same seed to bpt_layer_bwd.               */
 } bpt_config;
 
 /* FFN activation: the exact-erf GELU of GPT models (default) or eq. (2)'s ReLU,

@@ -28,7 +28,8 @@ c_i64, c_i32, c_f32, c_sz, c_vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_float
 class Config(ctypes.Structure):
     _fields_ = [("B", c_i64), ("S", c_i64), ("D", c_i64), ("H", c_i64), ("F", c_i64), ("Bq", c_i64),
                 ("Bkv", c_i64), ("causal", c_i32), ("dtype", c_i32), ("out_dtype", c_i32),
-                ("group_blocks", c_i32), ("ln_eps", c_f32), ("activation", c_i32)]
+                ("group_blocks", c_i32), ("ln_eps", c_f32), ("activation", c_i32), ("dropout", c_f32),
+                ("dropout_seed", ctypes.c_uint64)]
 
 
 PARAM_FIELDS = ("ln1_g", "ln1_b", "Wq", "Wk", "Wv", "Wo", "ln2_g", "ln2_b", "W1", "b1", "W2", "b2")
@@ -147,11 +148,12 @@ def _check(status: int) -> None:
 
 def make_config(B: int, S: int, D: int, H: int, F: int, Bq: int, Bkv: int, causal: bool = True,
                 dtype: str = "bf16", out_dtype: Optional[str] = None, group_blocks: int = 0,
-                ln_eps: float = 1e-5, activation: str = "gelu") -> Config:
+                ln_eps: float = 1e-5, activation: str = "gelu", dropout: float = 0.0,
+                dropout_seed: int = 0) -> Config:
     dt = {"f32": BPT_F32, "bf16": BPT_BF16}
     act = {"gelu": BPT_GELU, "relu": BPT_RELU}
     return Config(B, S, D, H, F, Bq, Bkv, int(bool(causal)), dt[dtype], dt[out_dtype or dtype],
-                  group_blocks, ln_eps, act[activation])
+                  group_blocks, ln_eps, act[activation], dropout, dropout_seed & (2 ** 64 - 1))
 
 
 def validate(cfg: Config) -> int:

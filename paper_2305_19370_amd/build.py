@@ -16,7 +16,7 @@ import tempfile
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
-SOURCES = ["libbpt.cpp", "gemm.hip", "attn_fwd.hip", "attn_bwd_dq.hip", "attn_bwd_dkdv.hip", "rowwise.hip", "gpt.hip"]
+SOURCES = ["libbpt.cpp", "gemm.hip", "attn_fwd.hip", "attn_bwd_dq.hip", "attn_bwd_dkdv.hip", "rowwise.hip", "gpt.hip", "dropout.hip"]
 # per-source code generation options: the attention kernels keep the accumulators of
 # their builtin MFMAs in architectural VGPRs (the default placement copies them
 # between register files every iteration; their long-lived accumulators are AGPRs

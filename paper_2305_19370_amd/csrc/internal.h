@@ -150,6 +150,21 @@ hipError_t adamw(Dt tl, float* p, const float* g, float* m, float* v, void* pl, 
 
 // out[i] (+)= sum over z < nz of part[z n + i], added in slice order (n % 4 == 0)
 hipError_t sum_slices(const float* part, int nz, int64_t n, float* out, int accumulate, hipStream_t s);
+// ---------------------------------------------------------------- residual-branch dropout
+// Element (t, n) of branch `site` is kept iff word n % 4 of Philox4x32-10 at counter
+// (n / 4, t, site, 0), key (k0, k1), is >= threshold; kept values are multiplied by scale.
+struct DropArgs {
+  uint32_t k0 = 0, k1 = 0, site = 0, threshold = 0;
+  float scale = 1.0f;
+  int64_t row0 = 0;            // token index t of the first row passed
+};
+// out = R + f * (acc + bias) over rows x D (acc fp32 [rows, D]; bias fp32 [D] or null)
+hipError_t dropout_add(const float* acc, Dt tr, const void* R, const float* bias, Dt to, void* out, int64_t rows,
+                       int64_t D, const DropArgs& a, hipStream_t s);
+// out = f * in over rows x D
+hipError_t dropout_scale(Dt ti, const void* in, Dt to, void* out, int64_t rows, int64_t D, const DropArgs& a,
+                         hipStream_t s);
+
 // bytes (a multiple of 4) of zeros at p, by a kernel (no memset node in captured graphs)
 hipError_t fill_zero(void* p, int64_t bytes, hipStream_t s);
 

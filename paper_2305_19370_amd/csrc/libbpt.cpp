@@ -41,6 +41,7 @@ size_t esize(int32_t dt) { return dt == BPT_BF16 ? 2 : 4; }
 struct Dims {
   int64_t B, S, D, H, F, dh, T, Sp, Tp, R, Rp;
   size_t E;
+  bool drop;             // residual-branch dropout on (rate > 0)
 };
 
 Dims dims_of(const bpt_config& c) {
@@ -48,6 +49,7 @@ Dims dims_of(const bpt_config& c) {
   d.B = c.B; d.S = c.S; d.D = c.D; d.H = c.H; d.F = c.F;
   d.dh = c.D / c.H;
   d.T = c.B * c.S;
+  d.drop = c.dropout > 0.0f;
   d.Sp = rup(c.S, 64);
   d.Tp = c.B * d.Sp;
   const int64_t g = c.group_blocks > 0 ? c.group_blocks
@@ -75,6 +77,8 @@ bpt_status check(const bpt_config* c) {
   if (!(c->ln_eps > 0.0f)) return fail(BPT_ERR_INVALID_ARG, "ln_eps must be > 0");
   if (c->activation != BPT_GELU && c->activation != BPT_RELU)
     return fail(BPT_ERR_INVALID_ARG, "activation must be BPT_GELU or BPT_RELU");
+  if (!(c->dropout >= 0.0f && c->dropout < 1.0f))
+    return fail(BPT_ERR_INVALID_ARG, "dropout rate must lie in [0, 1)");
   const int64_t dh = c->D / c->H;
   if (dh != 64 && dh != 128)
     return fail(BPT_ERR_UNSUPPORTED, "head dim D/H=%lld unsupported (64 or 128)", (long long)dh);
@@ -123,6 +127,7 @@ SavedPtrs saved_layout(const Dims& d, void* base, int64_t* total) {
 
 struct FwdWs {
   void *u, *vg, *gg;
+  float* acc;            // FFN output of a group before its dropout (null: no dropout)
 };
 
 FwdWs fwd_ws(const Dims& d, void* base, int64_t* total) {
@@ -131,6 +136,7 @@ FwdWs fwd_ws(const Dims& d, void* base, int64_t* total) {
   w.u = bp.take(d.T * d.D * d.E);
   w.vg = bp.take(d.R * d.D * d.E);
   w.gg = bp.take(d.R * d.F * d.E);
+  w.acc = d.drop ? (float*)bp.take(d.R * d.D * 4) : nullptr;
   *total = rup(bp.off, kAlign);
   return w;
 }
@@ -142,6 +148,7 @@ struct BwdWs {
   float *dv, *dh, *dU, *ndelta, *nlse2, *partial, *scratch;
   void *dhe, *dhT, *dO, *dqkvT, *u;
   float* kpart;          // K-slice partials of the D x D weight gradients (null: no split)
+  void* dYm;             // dY through the FFN branch's dropout (null: no dropout)
 };
 
 // Slices of K for a D x D weight-gradient GEMM (fp32 C, plain store) whose 256 x 256 tile
@@ -179,8 +186,22 @@ BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
   w.scratch = (float*)bp.take(2 * std::max(d.D, d.F) * 4);
   const int kz = ksplit(d.D, d.S);
   w.kpart = kz > 1 ? (float*)bp.take(kz * d.D * d.D * 4) : nullptr;
+  w.dYm = d.drop ? bp.take(d.T * d.D * d.E) : nullptr;
   *total = rup(bp.off, kAlign);
   return w;
+}
+
+// the dropout masks' generator key, threshold and scale for branch `site`
+DropArgs drop_args(const bpt_config& c, uint32_t site, int64_t row0) {
+  DropArgs a;
+  a.k0 = (uint32_t)(c.dropout_seed & 0xFFFFFFFFu);
+  a.k1 = (uint32_t)(c.dropout_seed >> 32);
+  a.site = site;
+  const double th = std::floor((double)c.dropout * 4294967296.0);
+  a.threshold = (uint32_t)std::min(th, 4294967295.0);
+  a.scale = (float)(1.0 / (1.0 - (double)c.dropout));
+  a.row0 = row0;
+  return a;
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
@@ -479,8 +500,16 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
       go.A = off(sv.o, t0 * D * E_); go.lda = D; go.B = p->Wo; go.ldb = D; go.trans_b = 1;
       go.C = sv.h + t0 * D; go.ldc = D; go.R = off(X, t0 * D * E_); go.ldr = D;
       go.M = r; go.N = D; go.K = D;
-      RUN("gemm.wo", gemm_flops(go), gemm_bytes(go, E_, 4) + (double)r * D * E_,
-          gemm(E, EPI_RESID, F32, E, go, s));
+      if (!d.drop) {
+        RUN("gemm.wo", gemm_flops(go), gemm_bytes(go, E_, 4) + (double)r * D * E_,
+            gemm(E, EPI_RESID, F32, E, go, s));
+      } else {   // O Wo into h, then h = X + drop(h) in place
+        go.R = nullptr;
+        RUN("gemm.wo", gemm_flops(go), gemm_bytes(go, E_, 4), gemm(E, EPI_STORE, F32, F32, go, s));
+        RUN("dropout.fwd", 0, (double)r * D * (8 + E_),
+            dropout_add(sv.h + t0 * D, E, off(X, t0 * D * E_), nullptr, F32, sv.h + t0 * D, r, D,
+                        drop_args(*cfg, 0, t0), s));
+      }
 
       RUN("layernorm.fwd", 0, (double)r * D * (4 + E_),
           layer_norm(F32, E, sv.h + t0 * D, D, p->ln2_g, p->ln2_b, w.vg, D, sv.mu2 + t0, sv.rstd2 + t0, r,
@@ -494,7 +523,14 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
       GemmArgs g2;     // Y = h + G W2 + b2
       g2.A = w.gg; g2.lda = F; g2.B = p->W2; g2.ldb = D; g2.trans_b = 1; g2.C = off(Y, t0 * D * EO);
       g2.ldc = D; g2.R = sv.h + t0 * D; g2.ldr = D; g2.bias = p->b2; g2.M = r; g2.N = D; g2.K = F;
-      RUN("gemm.ffn2", gemm_flops(g2), gemm_bytes(g2, E_, EO) + 4.0 * r * D, gemm(E, EPI_RESID, OUT, F32, g2, s));
+      if (!d.drop) {
+        RUN("gemm.ffn2", gemm_flops(g2), gemm_bytes(g2, E_, EO) + 4.0 * r * D, gemm(E, EPI_RESID, OUT, F32, g2, s));
+      } else {   // G W2 into fp32 workspace, then Y = h + drop(. + b2)
+        g2.C = w.acc; g2.R = nullptr; g2.bias = nullptr;
+        RUN("gemm.ffn2", gemm_flops(g2), gemm_bytes(g2, E_, 4), gemm(E, EPI_STORE, F32, F32, g2, s));
+        RUN("dropout.fwd", 0, (double)r * D * (8 + EO),
+            dropout_add(w.acc, F32, sv.h + t0 * D, p->b2, OUT, off(Y, t0 * D * EO), r, D, drop_args(*cfg, 1, t0), s));
+      }
     }
   }
   return BPT_OK;
@@ -542,10 +578,16 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
 
   // ---- FFN and LN2 backward, per group of query blocks, recomputing the FFN intermediate
   bool first = true;
+  // the FFN branch sees dY through its dropout; the residual path sees dY itself
+  const void* dYf = dY;
+  if (d.drop) {
+    RUN("dropout.bwd", 0, (double)T * D * 2 * E_, dropout_scale(E, dY, E, w.dYm, T, D, drop_args(*cfg, 1, 0), s));
+    dYf = w.dYm;
+  }
   for (int64_t b = 0; b < d.B; ++b) {
     for (int64_t s0 = 0; s0 < S; s0 += d.R) {
       const int64_t r = std::min(d.R, S - s0), rp = rup(r, 64), t0 = b * S + s0;
-      const void* dYg = off(dY, t0 * D * E_);
+      const void* dYg = off(dYf, t0 * D * E_);
       RUN("layernorm.fwd", 0, (double)r * D * (4 + E_),
           layer_norm(F32, E, sv.h + t0 * D, D, p->ln2_g, p->ln2_b, w.vg, D, sv.mu2 + t0, sv.rstd2 + t0, r, D,
                      cfg->ln_eps, 1, s));
@@ -593,7 +635,9 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     RUN("reduce.layernorm", 0, (double)T * D * 8,
         layer_norm_param_grad(F32, sv.h, sv.mu2, sv.rstd2, w.dv, G.dln2_g ? G.dln2_g : w.scratch,
                               G.dln2_b ? G.dln2_b : w.scratch + D, w.partial, T, D, s));
-  if (G.db2) RUN("reduce.bias", 0, (double)T * D * E_, col_sum(E, dY, D, T, D, G.db2, 0, w.partial, s));
+  if (G.db2) RUN("reduce.bias", 0, (double)T * D * E_, col_sum(E, dYf, D, T, D, G.db2, 0, w.partial, s));
+  if (d.drop)   // the output projection sees dh through its dropout
+    RUN("dropout.bwd", 0, (double)T * D * (4 + E_), dropout_scale(F32, w.dh, E, w.dhe, T, D, drop_args(*cfg, 0, 0), s));
 
   // ---- output projection backward: dO = dh Wo^T, dWo = O^T dh
   {

@@ -22,6 +22,7 @@ import torch
 
 from bpt_inputs import WORKLOADS, make_inputs, small_workload
 from gpu_util import GRAD_NAMES, bf16_model, run_gpu, run_oracle, say, stats, table
+import oracle
 
 pytestmark = pytest.mark.gpu
 
@@ -207,3 +208,32 @@ def test_bf16_workload_1b_s4096():
     gpu = run_gpu(w, inp)
     Yr, _, g = run_oracle(w, inp)
     compare_all(w, inp, gpu, Yr, g, "bf16", w.name)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_residual_dropout(dtype):
+    """Dropout (rate 0.1) on both residual branches: the GPU regenerates the oracle's
+    Philox masks exactly (a wrong mask shows as O(1) errors), ragged groups over two
+    sequences so the token index crosses group and sequence boundaries. fp32: the fp32
+    gate; bf16: e_mean <= 1e-2 and e_max <= 6e-2 (the bf16 rounding floor without
+    dropout is e_mean <= 5e-3, e_max <= 2.3e-2; kept values grow by 1/(1-p))."""
+    w = small_workload(dtype, B=2, S=250, D=256, H=2, F=512, causal=True, Bq=64, Bkv=64)
+    inp = make_inputs(w, seed=9, affine=True, biases=True)
+    p, seed = 0.1, 0x0123456789ABCDEF
+    say(f"case dropout {w.name} p={p}")
+    gpu = run_gpu(w, inp, group_blocks=2, dropout=p, dropout_seed=seed)
+    prm = oracle.params_from_inputs(inp)
+    prm.dropout, prm.dropout_seed = p, seed
+    Yr, cache = oracle.layer_fwd(inp["X"].double().numpy(), prm, w.H, w.causal)
+    g = oracle.layer_bwd(cache, prm, inp["dY"].double().numpy())
+    if dtype == "f32":
+        compare_all(w, inp, gpu, Yr, g, "fp32", w.name + "_dropout")
+        return
+    rows, bad = [], []
+    for n in ["Y", "dX"] + [k for k in GRAD_NAMES if k in gpu]:
+        s = stats(gpu[n].numpy(), Yr if n == "Y" else g[n])
+        rows.append((n, s))
+        if not (s["e_mean"] <= 1e-2 and s["e_max"] <= 6e-2):
+            bad.append(n)
+    say(f"\n[{w.name}_dropout]\n" + table(rows))
+    assert not bad, bad
