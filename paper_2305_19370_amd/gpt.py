@@ -47,6 +47,8 @@ class GPTShape:
     causal: bool = True
     ln_eps: float = 1e-5
     xent_block_rows: int = 0       # 0 = the library's default
+    dropout: float = 0.0           # residual-branch dropout rate of every layer
+    dropout_seed: int = 0          # base of the per-layer, per-step mask keys
 
     @property
     def ldw(self) -> int:
@@ -86,7 +88,8 @@ class GPT:
         self.tdt = torch.bfloat16 if s.dtype == "bf16" else torch.float32
         lowp = torch.bfloat16 if s.dtype == "bf16" else None
         self.cfg = bpt.make_config(s.B, s.S, s.D, s.H, s.F, s.Bq, s.Bkv, causal=s.causal, dtype=s.dtype,
-                                   out_dtype=s.dtype, ln_eps=s.ln_eps, activation=s.activation)
+                                   out_dtype=s.dtype, ln_eps=s.ln_eps, activation=s.activation,
+                                   dropout=s.dropout)
         bpt._check(bpt.validate(self.cfg))
         T = s.B * s.S
         self.xcfg = bpt.make_xent_config(T, s.D, s.V, ldw=s.ldw, block_rows=s.xent_block_rows, dtype=s.dtype)
@@ -181,12 +184,19 @@ class GPT:
         return out
 
     # ------------------------------------------------------------ step
+    def _layer_cfg(self, l: int) -> bpt.Config:
+        """The layer config with layer l's dropout key for the current step (forward and
+        backward of one step use the same key; every layer and step a different one)."""
+        if self.shape.dropout > 0.0:
+            self.cfg.dropout_seed = (self.shape.dropout_seed + (self.step_count << 20) + l) & (2 ** 64 - 1)
+        return self.cfg
+
     def forward(self, tokens: torch.Tensor, targets: torch.Tensor, saving: bool = True) -> torch.Tensor:
         """Loss (a one-element fp32 tensor) of tokens [B*S] int32 with targets [B*S] int32."""
         s = self.shape
         bpt.embed_fwd(self.ecfg, tokens, self.weight("Wte"), self.weight("Wpe") if s.pos_table else None, self.X[0])
         for l in range(s.L):
-            bpt.layer_fwd(self.cfg, self.X[l], self.layer_params(l), self.X[l + 1], self.saved[l], self.ws)
+            bpt.layer_fwd(self._layer_cfg(l), self.X[l], self.layer_params(l), self.X[l + 1], self.saved[l], self.ws)
         bpt.ln_fwd(self.lcfg, self.X[s.L], self.master("lnf_g"), self.master("lnf_b"), self.hf, self.mean, self.rstd)
         bpt.xent_fwd(self.xcfg, self.hf, self.weight("Wout"), targets, self.loss, self.lse, self.ws)
         return self.loss
@@ -200,7 +210,7 @@ class GPT:
         bpt.ln_bwd(self.lcfg, self.X[s.L], self.master("lnf_g"), self.mean, self.rstd, self.dh, cur,
                    self.grad("lnf_g"), self.grad("lnf_b"), self.ws)
         for l in range(s.L - 1, -1, -1):
-            bpt.layer_bwd(self.cfg, self.X[l], self.layer_params(l), self.saved[l], cur, nxt, self.layer_grads(l),
+            bpt.layer_bwd(self._layer_cfg(l), self.X[l], self.layer_params(l), self.saved[l], cur, nxt, self.layer_grads(l),
                           self.ws)
             cur, nxt = nxt, cur
         bpt.embed_bwd(self.ecfg, tokens, cur, self.grad("Wte"), self.grad("Wpe") if s.pos_table else None)

@@ -172,6 +172,19 @@ def test_activation_is_validated():
     assert bpt.validate(cfg) == 1
 
 
+def test_dropout_is_validated_and_sizes_its_workspace():
+    """A rate outside [0, 1) is rejected; a rate > 0 adds the fp32 FFN-output block
+    (forward) and the masked dY (backward) to the workspaces."""
+    base = bpt.make_config(1, 256, 256, 2, 512, 64, 64, True, "bf16")
+    drop = bpt.make_config(1, 256, 256, 2, 512, 64, 64, True, "bf16", dropout=0.1, dropout_seed=2 ** 64 - 1)
+    assert bpt.validate(drop) == 0
+    assert bpt.workspace_bytes(drop, False) > bpt.workspace_bytes(base, False)
+    assert bpt.workspace_bytes(drop, True) >= bpt.workspace_bytes(base, True) + 256 * 256 * 2
+    for bad in (1.0, -0.1, float("nan")):
+        drop.dropout = bad
+        assert bpt.validate(drop) == 1
+
+
 def test_gpt_step_entries_validate_before_launch():
     """Embedding, final LayerNorm and AdamW reject bad configurations and pointers
     on the host (fake, never-dereferenced addresses; nothing launches)."""
