@@ -272,6 +272,8 @@ def bench_gpt(args) -> int:
     shp = dict(GPT_SHAPE)
     if args.gpt_seq:
         shp["S"] = args.gpt_seq
+    if args.gpt_batch:
+        shp["B"] = args.gpt_batch
     s = GPTShape(**shp, dtype="bf16")
     torch.cuda.set_device(0)
     print(f"[bench] gpt {s}", file=sys.stderr, flush=True)
@@ -316,7 +318,7 @@ def bench_gpt(args) -> int:
         achieved = rec["bytes"] / (rec["ms"] / 1e3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM_GBS}
-    workload = f"gpt_xl_1b_s{s.S}"
+    workload = f"gpt_xl_1b_s{s.S}" + (f"_b{s.B}" if s.B != 1 else "")
     roof.update({"kernel": name, "launches_per_step": rec["count"] / args.steps,
                  "avg_launch_ms": rec["ms"] / rec["count"], "traffic": recorded_traffic(name, workload),
                  "traffic_unit": "bytes per launch"})
@@ -361,6 +363,7 @@ def main() -> int:
     ap.add_argument("--gpt", action="store_true",
                     help="measure a GPT-XL (1B) training step (24 layers, head, AdamW) instead of the layer")
     ap.add_argument("--gpt-seq", type=int, default=0, help="sequence length of --gpt (default 16384)")
+    ap.add_argument("--gpt-batch", type=int, default=0, help="sequences per step of --gpt (default 1)")
     args = ap.parse_args()
     if args.copy_probe:
         return copy_probe(args.copy_probe, 3)
