@@ -151,16 +151,16 @@ struct BwdWs {
   void* dYm;             // dY through the FFN branch's dropout (null: no dropout)
 };
 
-// Slices of K for a D x D weight-gradient GEMM (fp32 C, plain store) whose 256 x 256 tile
-// grid would leave most of the 256 CUs idle (D < 4096): the slices run as batch entries
-// into fp32 partials that sum_slices adds into C in a fixed order. Needs S % 64 == 0 (then
-// every slice is whole sequence rows and a multiple of the 32-deep K step).
+// Slices of K for a D x D weight-gradient GEMM (fp32 C, plain store) over K tokens whose
+// 256 x 256 tile grid would leave most of the 256 CUs idle (D < 4096): the slices run as
+// batch entries into fp32 partials that sum_slices adds into C in a fixed order. Needs
+// K % 64 == 0 (every slice a multiple of the 32-deep K step).
 constexpr int kMaxKSplit = 4;
-int ksplit(int64_t D, int64_t S) {
-  if (S % 64 != 0) return 1;
+int ksplit(int64_t D, int64_t K) {
+  if (K % 64 != 0) return 1;
   const int64_t tiles = ((D + 255) / 256) * ((D + 255) / 256);
   int z = 1;
-  while (z < kMaxKSplit && tiles * 2 * z <= 256 && S % (64 * 2 * z) == 0) z *= 2;
+  while (z < kMaxKSplit && tiles * 2 * z <= 256 && K % (64 * 2 * z) == 0) z *= 2;
   return z;
 }
 
@@ -184,7 +184,7 @@ BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
   w.dU = (float*)bp.take(d.T * d.D * 4);
   w.partial = (float*)bp.take((int64_t)layer_norm_param_grad_ws(std::max(d.D, d.F)) * 4);
   w.scratch = (float*)bp.take(2 * std::max(d.D, d.F) * 4);
-  const int kz = ksplit(d.D, d.S);
+  const int kz = d.S % 64 == 0 ? ksplit(d.D, d.T) : 1;   // the whole-batch GEMMs below
   w.kpart = kz > 1 ? (float*)bp.take(kz * d.D * d.D * 4) : nullptr;
   w.dYm = d.drop ? bp.take(d.T * d.D * d.E) : nullptr;
   *total = rup(bp.off, kAlign);
@@ -645,21 +645,31 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     g.A = w.dhe; g.lda = D; g.B = p->Wo; g.ldb = D; g.C = w.dO; g.ldc = D; g.M = T; g.N = D; g.K = D;
     RUN("gemm.bwd_do", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
   }
-  const int kz = w.kpart ? ksplit(D, S) : 1;
-  if (G.dWo && S % 32 == 0) {   // per sequence: O and dh both read token-major (K = S exactly)
+  // With S % 64 == 0 every sequence is whole 64-token rows (Sp == S): O, dh and u are
+  // token-major and the feature-major dQ^T, dK^T, dV^T unpadded over the whole batch, so
+  // each D x D weight gradient is one GEMM with K = T (split along K when D < 4096).
+  const bool whole = S % 64 == 0;
+  const int kz = whole && w.kpart ? ksplit(D, T) : 1;
+  auto wgrad = [&](const char* name, GemmArgs g, float* out, int64_t sa, int64_t sb) -> bpt_status {
+    if (kz > 1) {   // K slices of T / kz tokens; A and B step by sa and sb elements per slice
+      g.batch = kz; g.K = T / kz; g.sA = sa * g.K; g.sB = sb * g.K; g.C = w.kpart; g.sC = D * D;
+    }
+    RUN(name, gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
+    if (kz > 1) RUN("reduce.ksplit", 0, (double)(kz + 1) * D * D * 4, sum_slices(w.kpart, kz, D * D, out, 0, s));
+    return BPT_OK;
+  };
+  if (G.dWo && whole) {
+    GemmArgs g;
+    g.A = sv.o; g.lda = D; g.trans_a = 1; g.B = w.dhe; g.ldb = D; g.trans_b = 1; g.C = G.dWo; g.ldc = D;
+    g.M = D; g.N = D; g.K = T;
+    if ((st = wgrad("gemm.bwd_dwo", g, G.dWo, D, D)) != BPT_OK) return st;
+  } else if (G.dWo && S % 32 == 0) {   // per sequence: O and dh both read token-major (K = S exactly)
     for (int b = 0; b < B; ++b) {
       GemmArgs g;
       g.A = off(sv.o, b * S * D * E_); g.lda = D; g.trans_a = 1;
       g.B = off(w.dhe, b * S * D * E_); g.ldb = D; g.trans_b = 1; g.C = G.dWo; g.ldc = D;
       g.M = D; g.N = D; g.K = S; g.accumulate = b > 0;
-      if (kz > 1) {   // K slices of S / kz tokens: A and B step by that many rows
-        g.batch = kz; g.K = S / kz; g.sA = g.K * D; g.sB = g.K * D;
-        g.C = w.kpart; g.sC = D * D; g.accumulate = 0;
-      }
       RUN("gemm.bwd_dwo", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
-      if (kz > 1)
-        RUN("reduce.ksplit", 0, (double)(kz + (b > 0 ? 2 : 1)) * D * D * 4,
-            sum_slices(w.kpart, kz, D * D, G.dWo, b > 0, s));
     }
   } else if (G.dWo) {   // O read token-major, dh from its zero-padded feature-major copy
     RUN("transpose.act", 0, tb * T * D, transpose(E, w.dhe, D, S * D, w.dhT, Tp, Sp, S, D, Sp, B, s));
@@ -698,19 +708,20 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     float* outs[3] = {G.dWq, G.dWk, G.dWv};
     for (int i = 0; i < 3; ++i) {
       if (!outs[i]) continue;
+      if (whole) {   // u rows and dQ^T / dK^T / dV^T columns contiguous over the batch
+        GemmArgs g;
+        g.A = w.u; g.lda = D; g.trans_a = 1;
+        g.B = off(w.dqkvT, i * D * Tp * E_); g.ldb = Tp; g.C = outs[i]; g.ldc = D;
+        g.M = D; g.N = D; g.K = T;
+        if ((st = wgrad("gemm.bwd_dwqkv", g, outs[i], D, 1)) != BPT_OK) return st;
+        continue;
+      }
       for (int b = 0; b < B; ++b) {
         GemmArgs g;
         g.A = off(w.u, b * S * D * E_); g.lda = D; g.trans_a = 1; g.a_rows = S;
         g.B = off(w.dqkvT, (i * D * Tp + b * Sp) * E_); g.ldb = Tp; g.C = outs[i]; g.ldc = D;
         g.M = D; g.N = D; g.K = Sp; g.accumulate = b > 0;
-        if (kz > 1) {   // Sp == S here: K slices of S / kz tokens, rows of A, columns of B
-          g.batch = kz; g.K = S / kz; g.a_rows = 0; g.sA = g.K * D; g.sB = g.K;
-          g.C = w.kpart; g.sC = D * D; g.accumulate = 0;
-        }
         RUN("gemm.bwd_dwqkv", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
-        if (kz > 1)
-          RUN("reduce.ksplit", 0, (double)(kz + (b > 0 ? 2 : 1)) * D * D * 4,
-              sum_slices(w.kpart, kz, D * D, outs[i], b > 0, s));
       }
     }
   }
