@@ -214,3 +214,27 @@ def test_final_layernorm(rows, D, dtype):
             assert (d <= 2.0 ** -8 * np.abs(r) + 1e-4 * np.sqrt(np.mean(r * r))).all(), name
     for name, got, r in (("dg", dg, rdg), ("db", db, rdb)):      # fp32 outputs
         assert stats(f64(got), r)["e_max"] <= 1e-5, (name, stats(f64(got), r))
+
+
+def test_gpt_step_f32_with_dropout():
+    """fp32 step with residual dropout 0.1 in every layer: layer l of step 0 uses key
+    dropout_seed + l, and the oracle given the same keys matches at the fp32 bound."""
+    s = GPTShape(L=2, B=2, S=128, D=256, H=4, F=512, V=300, Bq=64, Bkv=64, dtype="f32", dropout=0.1,
+                 dropout_seed=0xABCDEF0123)
+    say(f"[gpt] dropout {s}")
+    m, inp = build(s, 5)
+    tok, tgt = inp["tokens"].to(DEV), inp["targets"].to(DEV)
+    loss = float(m.forward(tok, tgt).item())
+    m.backward(tok, tgt)
+    torch.cuda.synchronize()
+    P = oracle_params(inp, s)
+    for l, lp in enumerate(P.layers):
+        lp.dropout, lp.dropout_seed = s.dropout, s.dropout_seed + l
+    ref = gpt_fwd_bwd(inp["tokens"].numpy().reshape(s.B, s.S), inp["targets"].numpy().reshape(s.B, s.S), P, s.H)
+    assert abs(loss - ref["loss"]) <= 1e-5 * abs(ref["loss"]), (loss, ref["loss"])
+    for name, g, r in grad_pairs(m, ref, s):
+        st = stats(f64(g), r)
+        assert st["e_max"] <= 1e-4, (name, st)
+    P0 = oracle_params(inp, s)           # without dropout the loss differs: the masks are live
+    assert abs(gpt_fwd_bwd(inp["tokens"].numpy().reshape(s.B, s.S), inp["targets"].numpy().reshape(s.B, s.S),
+                           P0, s.H, backward=False)["loss"] - loss) > 1e-4
