@@ -270,17 +270,38 @@ __global__ __launch_bounds__(256) void ln_param_partial_kernel(const TI* x, cons
   partial[(int64_t)(kChunks + blockIdx.y) * D + d] = sb;
 }
 
+// Second stage: out0[d] (+)= sum_c partial[c D + d] and out1[d] (+)= sum_c partial[(kChunks + c) D + d].
+// A block of four waves per 64 columns; wave w sums chunks w, w + 4, ... (eight loads in flight
+// per lane) and the four wave sums are added through LDS in wave order.
 __global__ __launch_bounds__(256) void chunk_reduce_kernel(const float* partial, float* out0,
                                                            float* out1, int64_t D, int accumulate) {
-  const int64_t d = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (d >= D) return;
+  __shared__ float red[2][4][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t d = (int64_t)blockIdx.x * 64 + lane;
+  const bool ok = d < D;
   float s0 = 0.0f, s1 = 0.0f;
-  for (int c = 0; c < kChunks; ++c) {
-    s0 += partial[(int64_t)c * D + d];
-    if (out1) s1 += partial[(int64_t)(kChunks + c) * D + d];
+  if (ok) {
+    for (int c0 = wv; c0 < kChunks; c0 += 32) {
+      float v0[8], v1[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int c = c0 + 4 * u;
+        v0[u] = c < kChunks ? partial[(int64_t)c * D + d] : 0.0f;
+        v1[u] = (out1 && c < kChunks) ? partial[(int64_t)(kChunks + c) * D + d] : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) { s0 += v0[u]; s1 += v1[u]; }
+    }
   }
-  if (out0) out0[d] = accumulate ? out0[d] + s0 : s0;
-  if (out1) out1[d] = accumulate ? out1[d] + s1 : s1;
+  red[0][wv][lane] = s0;
+  red[1][wv][lane] = s1;
+  __syncthreads();
+  if (wv == 0 && ok) {
+    s0 = ((red[0][0][lane] + red[0][1][lane]) + red[0][2][lane]) + red[0][3][lane];
+    s1 = ((red[1][0][lane] + red[1][1][lane]) + red[1][2][lane]) + red[1][3][lane];
+    if (out0) out0[d] = accumulate ? out0[d] + s0 : s0;
+    if (out1) out1[d] = accumulate ? out1[d] + s1 : s1;
+  }
 }
 
 template <typename T>
@@ -325,46 +346,68 @@ __global__ __launch_bounds__(64) void col_partial8_kernel(const T* in, int64_t l
   Vec8<float>::store(partial + (int64_t)blockIdx.y * cols + c, s);
 }
 
+// LayerNorm parameter partials, wide form: a block of four waves per (512-column group, row
+// chunk); wave w sums the w-th quarter of the chunk's rows (8 columns per lane, 16-byte
+// loads, two rows in flight), and the four quarter sums are added through LDS in wave order.
 template <typename TI>
-__global__ __launch_bounds__(64) void ln_param_partial8_kernel(const TI* x, const float* mu, const float* rstd,
-                                                               const float* dout, float* partial, int64_t rows,
-                                                               int64_t D) {
-  const int64_t d = ((int64_t)blockIdx.x * 64 + threadIdx.x) * 8;
-  if (d >= D) return;
+__global__ __launch_bounds__(256) void ln_param_partial8_kernel(const TI* x, const float* mu, const float* rstd,
+                                                                const float* dout, float* partial, int64_t rows,
+                                                                int64_t D) {
+  __shared__ float red[2][4][64 * 8];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t d = ((int64_t)blockIdx.x * 64 + lane) * 8;
+  const bool ok = d < D;
   const int64_t per = (rows + kChunks - 1) / kChunks;
-  const int64_t r0 = blockIdx.y * per, r1 = r0 + per < rows ? r0 + per : rows;
+  const int64_t c0 = blockIdx.y * per, c1 = c0 + per < rows ? c0 + per : rows;
+  const int64_t q = (per + 3) / 4;
+  const int64_t r0 = c0 + wv * q, r1 = r0 + q < c1 ? r0 + q : c1;
   float sg[8] = {0, 0, 0, 0, 0, 0, 0, 0}, sb[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  int64_t r = r0;
-  for (; r + 2 <= r1; r += 2) {
-    float xv[2][8], dv[2][8];
+  if (ok) {
+    int64_t r = r0;
+    for (; r + 2 <= r1; r += 2) {
+      float xv[2][8], dv[2][8];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      Vec8<TI>::load(x + (r + u) * D + d, xv[u]);
-      Vec8<float>::load(dout + (r + u) * D + d, dv[u]);
+      for (int u = 0; u < 2; ++u) {
+        Vec8<TI>::load(x + (r + u) * D + d, xv[u]);
+        Vec8<float>::load(dout + (r + u) * D + d, dv[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const float m = mu[r + u], rs = rstd[r + u];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          sg[e] = fmaf(dv[u][e], (xv[u][e] - m) * rs, sg[e]);
+          sb[e] += dv[u][e];
+        }
+      }
     }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const float m = mu[r + u], rs = rstd[r + u];
+    for (; r < r1; ++r) {
+      float xv[8], dv[8];
+      Vec8<TI>::load(x + r * D + d, xv);
+      Vec8<float>::load(dout + r * D + d, dv);
+      const float m = mu[r], rs = rstd[r];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        sg[e] = fmaf(dv[u][e], (xv[u][e] - m) * rs, sg[e]);
-        sb[e] += dv[u][e];
+        sg[e] = fmaf(dv[e], (xv[e] - m) * rs, sg[e]);
+        sb[e] += dv[e];
       }
     }
   }
-  for (; r < r1; ++r) {
-    float xv[8], dv[8];
-    Vec8<TI>::load(x + r * D + d, xv);
-    Vec8<float>::load(dout + r * D + d, dv);
-    const float m = mu[r], rs = rstd[r];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    red[0][wv][lane * 8 + e] = sg[e];
+    red[1][wv][lane * 8 + e] = sb[e];
+  }
+  __syncthreads();
+  if (wv == 0 && ok) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      sg[e] = fmaf(dv[e], (xv[e] - m) * rs, sg[e]);
-      sb[e] += dv[e];
+      sg[e] = ((red[0][0][lane * 8 + e] + red[0][1][lane * 8 + e]) + red[0][2][lane * 8 + e]) + red[0][3][lane * 8 + e];
+      sb[e] = ((red[1][0][lane * 8 + e] + red[1][1][lane * 8 + e]) + red[1][2][lane * 8 + e]) + red[1][3][lane * 8 + e];
     }
+    Vec8<float>::store(partial + (int64_t)blockIdx.y * D + d, sg);
+    Vec8<float>::store(partial + (int64_t)(kChunks + blockIdx.y) * D + d, sb);
   }
-  Vec8<float>::store(partial + (int64_t)blockIdx.y * D + d, sg);
-  Vec8<float>::store(partial + (int64_t)(kChunks + blockIdx.y) * D + d, sb);
 }
 
 template <typename T>
@@ -600,7 +643,7 @@ hipError_t layer_norm_param_grad(Dt ti, const void* x, const float* mu, const fl
                                  int64_t rows, int64_t D, hipStream_t s) {
   if (D % 8 == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)dout & 15) == 0 && ((uintptr_t)partial & 15) == 0) {
     const dim3 grid8((unsigned)((D + 511) / 512), kChunks);
-    BPT_T(ti, TI, hipLaunchKernelGGL((ln_param_partial8_kernel<TI>), grid8, dim3(64), 0, s, (const TI*)x,
+    BPT_T(ti, TI, hipLaunchKernelGGL((ln_param_partial8_kernel<TI>), grid8, dim3(256), 0, s, (const TI*)x,
                                      mu, rstd, dout, partial, rows, D));
   } else {
     const dim3 grid((unsigned)((D + 255) / 256), kChunks);
@@ -609,7 +652,7 @@ hipError_t layer_norm_param_grad(Dt ti, const void* x, const float* mu, const fl
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)((D + 255) / 256)), dim3(256), 0, s, partial,
+  hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)((D + 63) / 64)), dim3(256), 0, s, partial,
                      dgamma, dbeta, D, 0);
   return hipGetLastError();
 }
@@ -627,7 +670,7 @@ hipError_t col_sum(Dt t, const void* in, int64_t ld, int64_t rows, int64_t cols,
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)((cols + 255) / 256)), dim3(256), 0, s, partial,
+  hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0, s, partial,
                      out, (float*)nullptr, cols, accumulate);
   return hipGetLastError();
 }
