@@ -348,6 +348,50 @@ def bench_gpt(args) -> int:
     return 0 if ok else 1
 
 
+# GEMM shapes (name, M, N, K, A transposed) of the 7B-shaped layer (T = 32768 tokens, D = 4096,
+# F = 16384, FFN groups of 8192 rows), as C[M, N] = A[M, K] B[K, N]
+YARDSTICK_SHAPES = (
+    ("qkv_proj", 32768, 4096, 4096, False),
+    ("ffn1", 8192, 16384, 4096, False),
+    ("ffn2", 8192, 4096, 16384, False),
+    ("dwqkv", 4096, 4096, 32768, True),
+    ("dw1", 4096, 16384, 8192, True),
+    ("du", 32768, 4096, 12288, False),
+)
+
+
+def gemm_yardstick(args) -> int:
+    """--gemm-yardstick: torch.matmul (hipBLASLt) in bf16 with fp32 accumulation on the
+    7B-shaped layer's GEMM shapes, then the libbpt layer step, in one process, so that
+    one counter pass sees the vendor GEMMs and the layer's kernels on the same box."""
+    import torch
+    torch.cuda.set_device(0)
+    g = torch.Generator(device="cpu").manual_seed(0)
+    res = {}
+    for name, M, N, K, at in YARDSTICK_SHAPES:
+        a = (torch.randn((K, M) if at else (M, K), generator=g) * 0.05).to(torch.bfloat16).cuda()
+        b = (torch.randn((K, N), generator=g) * 0.05).to(torch.bfloat16).cuda()
+        A = a.t() if at else a
+        for _ in range(3):
+            c = torch.matmul(A, b)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            c = torch.matmul(A, b)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        res[name] = {"M": M, "N": N, "K": K, "a_transposed": at, "ms": round(ms, 4),
+                     "tflops": round(2.0 * M * N * K / (ms / 1e3) / 1e12, 1)}
+        print(f"[yardstick] torch.matmul {name} {M}x{N}x{K}: {ms:.3f} ms, {res[name]['tflops']} TFLOP/s",
+              file=sys.stderr, flush=True)
+        del a, b, c, A
+    torch.cuda.empty_cache()
+    print(json.dumps({"yardstick": "torch.matmul bf16 (hipBLASLt)", "shapes": res}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -364,6 +408,8 @@ def main() -> int:
                     help="measure a GPT-XL (1B) training step (24 layers, head, AdamW) instead of the layer")
     ap.add_argument("--gpt-seq", type=int, default=0, help="sequence length of --gpt (default 16384)")
     ap.add_argument("--gpt-batch", type=int, default=0, help="sequences per step of --gpt (default 1)")
+    ap.add_argument("--gemm-yardstick", action="store_true",
+                    help="time torch.matmul (hipBLASLt) on the 7B-shaped layer's GEMM shapes, then run the layer")
     args = ap.parse_args()
     if args.copy_probe:
         return copy_probe(args.copy_probe, 3)
@@ -375,6 +421,10 @@ def main() -> int:
         return bench_xent(args)
     if args.gpt:
         return bench_gpt(args)
+    if args.gemm_yardstick:
+        rc = gemm_yardstick(args)
+        if rc:
+            return rc
 
     import torch
     from bpt_inputs import WORKLOADS, make_inputs
