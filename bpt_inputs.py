@@ -73,6 +73,25 @@ WORKLOADS: Dict[str, Workload] = {
     ]
 }
 
+# The 13B-shaped layer's sequence-length sweep (linear memory in S): same shape and
+# blocks at shorter sequences.
+SWEEP_S = (8192, 16384, 32768, 65536)
+
+
+def sweep_workload(S: int) -> Workload:
+    base = WORKLOADS["bf16_13b_s65536"]
+    return base.with_(S=S, name=f"bf16_13b_s{S}", note=f"GPT 13B-shaped layer at S={S} (sweep)")
+
+
+def workload(name: str) -> Workload:
+    """A named workload: one of WORKLOADS, or bf16_13b_s<S> for a length of the sweep."""
+    if name in WORKLOADS:
+        return WORKLOADS[name]
+    if name.startswith("bf16_13b_s") and name[len("bf16_13b_s"):].isdigit():
+        return sweep_workload(int(name[len("bf16_13b_s"):]))
+    raise KeyError(name)
+
+
 TENSOR_ORDER = ("X", "Wq", "Wk", "Wv", "Wo", "W1", "W2", "dY")
 
 

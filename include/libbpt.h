@@ -58,10 +58,14 @@ typedef enum { BPT_F32 = 0, BPT_BF16 = 1 } bpt_dtype;
 
 typedef struct {
   int64_t B, S, D, H, F;   /* batch, sequence length, model width, heads, FFN width        */
-  int64_t Bq, Bkv;         /* query / key-value block LENGTHS in tokens (Section 3). Need  */
-                           /* not divide S. Bq is the unit of FFN fusion; Bkv is the KV   */
-                           /* step of the method. Results depend on them only through     */
-                           /* rounding (the method is exact).                              */
+  int64_t Bq, Bkv;         /* query / key-value block LENGTHS in tokens (Section 3's      */
+                           /* problem statement, Algorithm 1). Need not divide S. Bq is   */
+                           /* the unit of FFN fusion (see group_blocks). Bkv is validated */
+                           /* but does not change the GPU path: its kernels step through  */
+                           /* keys in tiles of 64, their LDS / matrix-core tile, whatever */
+                           /* Bkv is (bpt_describe reports the tiles). The method is      */
+                           /* exact, so results depend on Bq and the tiles only through   */
+                           /* rounding.                                                     */
   int32_t causal;          /* 1: query q sees key k iff k <= q, within one sequence        */
   int32_t dtype;           /* bpt_dtype of X, dY, weights and saved activations             */
   int32_t out_dtype;       /* bpt_dtype of Y and dX                                         */
@@ -116,13 +120,18 @@ bpt_status bpt_validate(const bpt_config* cfg);
  * clipped to S). Returns -1 for an invalid configuration. Host-only. */
 int64_t bpt_group_rows(const bpt_config* cfg);
 
-/* Size of the `saved` buffer and the offsets inside it. O(B*S*D); no S*S or S*F
- * term. Returns 0 / a non-OK status for an invalid configuration. Host-only. */
+/* Size of the `saved` buffer and the offsets inside it. Section 3.1's memory analysis
+ * counts what a blockwise layer keeps for its backward: activations linear in the
+ * sequence length, no S x S attention matrix and no S x F FFN intermediate. Here that
+ * is O(B*S*D) (layout below). Returns 0 / a non-OK status for an invalid
+ * configuration. Host-only. */
 size_t bpt_saved_bytes(const bpt_config* cfg);
 bpt_status bpt_saved_layout_of(const bpt_config* cfg, bpt_saved_layout* out);
 
 /* Workspace needed by bpt_layer_fwd (backward = 0) or bpt_layer_bwd (backward = 1):
- * O(D^2 + D*F + B*S*D + group_rows*F). Returns 0 for an invalid configuration. Host-only. */
+ * O(D^2 + D*F + B*S*D + group_rows*F). Section 3.1 bounds the live FFN intermediate of a
+ * blockwise layer by one query block's [Bq, F]; here it is one group's [group_rows, F],
+ * independent of S. Returns 0 for an invalid configuration. Host-only. */
 size_t bpt_workspace_bytes(const bpt_config* cfg, int backward);
 
 /* Forward of one layer (Algorithm 1). X, Y: [B, S, D]. `saved` (bpt_saved_bytes
@@ -132,11 +141,24 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
 
 /* Backward of one layer given the forward's `saved` buffer and the upstream
  * gradient dY [B, S, D]. Writes dX [B, S, D] (out_dtype) and every non-NULL
- * gradient in `grads`. Attention probabilities are rebuilt blockwise from the
- * saved log-sum-exp; the FFN intermediate is recomputed per query-block group. */
+ * gradient in `grads`. As in Section 3 (the checkpointed attention scan and the
+ * rematerialised FFN of Fig. 3), nothing of size S x S or S x F was saved: attention
+ * probabilities are rebuilt blockwise from the saved log-sum-exp, and the FFN
+ * intermediate is recomputed per query-block group. Same conventions as the forward;
+ * the workspace must be bpt_workspace_bytes(cfg, 1) bytes. */
 bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params* params,
                          const void* saved, const void* dY, void* dX, const bpt_grads* grads,
                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Where bpt_layer_bwd leaves the gradients of the attention inputs inside its workspace,
+ * for tests and tooling (the attention backward of Section 3 rebuilds the probabilities
+ * blockwise and produces them on the way to dU and the projection weight gradients).
+ * After the call has completed, the workspace bytes from *offset hold dQ, dK, dV
+ * feature-major as one [3D, B*Sp] matrix in cfg->dtype, Sp = S rounded up to 64:
+ * element (b, s, n) of dQ at row n, column b*Sp + s; dK in rows [D, 2D), dV in rows
+ * [2D, 3D); columns b*Sp + s with s >= S hold zeros. dQ, dK, dV are the gradients of the
+ * unscaled Q = U Wq, K, V (the base-2 scale of the stored query is undone). Host-only. */
+bpt_status bpt_bwd_qkv_grad_offset(const bpt_config* cfg, size_t* offset);
 
 const char* bpt_status_string(int status);
 const char* bpt_last_error(void);

@@ -72,7 +72,7 @@ EXPORTS = ("bpt_validate", "bpt_group_rows", "bpt_saved_bytes", "bpt_saved_layou
            "bpt_layer_fwd", "bpt_layer_bwd", "bpt_status_string", "bpt_last_error", "bpt_describe",
            "bpt_profile_enable", "bpt_profile_report", "bpt_xent_validate", "bpt_xent_workspace_bytes",
            "bpt_xent_fwd", "bpt_xent_bwd", "bpt_embed_fwd", "bpt_embed_bwd", "bpt_ln_workspace_bytes",
-           "bpt_ln_fwd", "bpt_ln_bwd", "bpt_adamw_step")
+           "bpt_ln_fwd", "bpt_ln_bwd", "bpt_adamw_step", "bpt_bwd_qkv_grad_offset")
 
 _lib = None
 
@@ -101,6 +101,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.bpt_layer_fwd.restype = c_i32
     lib.bpt_layer_bwd.argtypes = [P(Config), c_vp, P(Params), c_vp, c_vp, c_vp, P(Grads), c_vp, c_sz, c_vp]
     lib.bpt_layer_bwd.restype = c_i32
+    lib.bpt_bwd_qkv_grad_offset.argtypes = [P(Config), P(c_sz)]
+    lib.bpt_bwd_qkv_grad_offset.restype = c_i32
     lib.bpt_status_string.argtypes = [c_i32]
     lib.bpt_status_string.restype = ctypes.c_char_p
     lib.bpt_last_error.argtypes = []
@@ -178,6 +180,12 @@ def saved_layout(cfg: Config) -> Dict[str, int]:
     return {n: getattr(out, n) for n in SAVED_FIELDS}
 
 
+def bwd_qkv_grad_offset(cfg: Config) -> int:
+    off = c_sz()
+    _check(load().bpt_bwd_qkv_grad_offset(ctypes.byref(cfg), ctypes.byref(off)))
+    return off.value
+
+
 def describe(cfg: Config) -> str:
     buf = ctypes.create_string_buffer(1024)
     load().bpt_describe(ctypes.byref(cfg), buf, 1024)
@@ -253,7 +261,10 @@ class Layer:
 
     def backward(self, X: torch.Tensor, params: Dict[str, Optional[torch.Tensor]], saved: torch.Tensor,
                  dY: torch.Tensor, want: Optional[Tuple[str, ...]] = None,
-                 workspace: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, Dict[str, torch.Tensor]]:
+                 workspace: Optional[torch.Tensor] = None,
+                 qkv_grads: bool = False) -> Tuple[torch.Tensor, Dict[str, torch.Tensor]]:
+        """dX and the parameter gradients; with qkv_grads, also "dQ", "dK", "dV" [B, S, D]
+        (copies of what the backward leaves in its workspace, bpt_bwd_qkv_grad_offset)."""
         D, F = self.cfg.D, self.cfg.F
         shapes = {"dln1_g": (D,), "dln1_b": (D,), "dWq": (D, D), "dWk": (D, D), "dWv": (D, D), "dWo": (D, D),
                   "dln2_g": (D,), "dln2_b": (D,), "dW1": (D, F), "db1": (F,), "dW2": (F, D), "db2": (D,)}
@@ -268,6 +279,14 @@ class Layer:
         dX = torch.empty(X.shape, dtype=self.out_dtype, device=self.device)
         ws = workspace if workspace is not None else self._bytes(workspace_bytes(self.cfg, True))
         layer_bwd(self.cfg, X, params, saved, dY, dX, grads, ws)
+        if qkv_grads:
+            c = self.cfg
+            E = _TORCH_DT[c.dtype]
+            Sp = (c.S + 63) // 64 * 64
+            off, n = bwd_qkv_grad_offset(c), 3 * c.D * c.B * Sp
+            m = ws[off:off + n * (2 if E == torch.bfloat16 else 4)].view(E).view(3, c.D, c.B, Sp)[..., :c.S]
+            for i, name in enumerate(("dQ", "dK", "dV")):
+                grads[name] = m[i].permute(1, 2, 0).contiguous()
         return dX, grads
 
     def saved_views(self, saved: torch.Tensor) -> Dict[str, torch.Tensor]:

@@ -365,6 +365,16 @@ size_t bpt_workspace_bytes(const bpt_config* cfg, int backward) {
   return (size_t)total;
 }
 
+bpt_status bpt_bwd_qkv_grad_offset(const bpt_config* cfg, size_t* offset) {
+  bpt_status st = check(cfg);
+  if (st != BPT_OK) return st;
+  if (!offset) return fail(BPT_ERR_INVALID_ARG, "offset is NULL");
+  int64_t total;
+  BwdWs w = bwd_ws(dims_of(*cfg), nullptr, &total);   // zero base: pointers are offsets
+  *offset = (size_t)(uintptr_t)w.dqkvT;
+  return BPT_OK;
+}
+
 const char* bpt_status_string(int st) {
   switch (st) {
     case BPT_OK: return "BPT_OK";

@@ -1,17 +1,23 @@
 """Writes the expected values of the full-size sampled parity tests — run on the CPU.
 
 For each long-context workload (the 7B-, RL- and 13B-shaped layers at their full
-sequence lengths) the float64 rows oracle (``oracle/rows.py``: the plain layer
-definition restricted to selected query rows) is evaluated on the seeded inputs
-of ``bpt_inputs.make_inputs(w, seed=0)`` with the upstream gradient equal to dY
-on the selected rows and zero elsewhere. Under that dY every gradient the rows
-oracle returns is the exact full backward value, so the GPU run (same inputs,
-same masked dY, full size) can be compared on:
+sequence lengths, and the 13B-shaped layer at two shorter lengths of its sweep) the
+float64 rows oracle (``oracle/rows.py``: the plain layer definition restricted to
+selected query rows) is evaluated on the seeded inputs of
+``bpt_inputs.make_inputs(w, seed=0)`` with the upstream gradient equal to dY on the
+selected rows and zero elsewhere. Under that dY every gradient the rows oracle
+returns is the exact full backward value, so the GPU run (same inputs, same masked
+dY, full size) can be compared on:
 
   * Y and dX at the selected rows (every element; errors normalised by the RMS of
     those rows of the reference);
   * dX and every weight / bias / LayerNorm gradient at 2048 sampled positions
-    (normalised by the RMS of the full reference tensor);
+    (errors normalised by the RMS of the reference at the sampled positions);
+
+The selected rows (about 270) are spread over the query tiles of three windows of
+one FFN group each: the first group, the middle of the sequence and the last group,
+plus the first and last two tokens, so that the attention backward sees nonzero
+gradients on query tiles of every part of the causal triangle.
 
 The bf16 rounding model restricted to the same rows (``oracle/bf16_rows.py``) is
 evaluated too, and its normalised errors on exactly these checks are stored: they
@@ -38,10 +44,25 @@ SEED = 0
 GRADS = ("dWq", "dWk", "dWv", "dWo", "dW1", "dW2", "db1", "db2", "dln1_g", "dln1_b", "dln2_g", "dln2_b")
 
 
+GROUP_ROWS = 8192          # rows of one FFN group of these workloads
+PER_WINDOW = 88
+
+
 def sample_rows(S: int) -> np.ndarray:
-    """First tokens, both sides of the first FFN-group boundary (8192 rows), the middle,
-    and the last two tokens of the sequence."""
-    return np.array(sorted({0, 1, 8191, 8192, S // 2 + 1, S - 2, S - 1}), dtype=np.int64)
+    """PER_WINDOW rows in each of three windows of GROUP_ROWS rows (first group, middle,
+    last group), one per stride of GROUP_ROWS / PER_WINDOW at a seeded offset inside the
+    stride, plus tokens 0, 1, S-2, S-1 and both sides of the first group boundary."""
+    rng = np.random.default_rng(S)
+    rows = {0, 1, S - 2, S - 1, GROUP_ROWS - 1, GROUP_ROWS}
+    for w0 in (0, max(0, S // 2 - GROUP_ROWS // 2), max(0, S - GROUP_ROWS)):
+        n = min(GROUP_ROWS, S - w0)
+        stride = n // PER_WINDOW
+        for i in range(PER_WINDOW):
+            rows.add(w0 + i * stride + int(rng.integers(0, stride)))
+    return np.array(sorted(r for r in rows if 0 <= r < S), dtype=np.int64)
+
+
+FULLSIZE = ("bf16_7b_s32768", "bf16_rl_s96000", "bf16_13b_s65536", "bf16_13b_s8192", "bf16_13b_s32768")
 
 
 def expected_path(name: str) -> str:
@@ -65,7 +86,7 @@ def checks(e, res):
             continue
         got = np.asarray(res[k])
         assert tuple(got.shape) == tuple(e[k + "_shape"]), (k, got.shape)
-        out.append((k, got.reshape(-1)[e[k + "_idx"]], e[k + "_val"], float(e[k + "_rms"])))
+        out.append((k, got.reshape(-1)[e[k + "_idx"]], e[k + "_val"], rms(e[k + "_val"])))
     return out
 
 
@@ -78,8 +99,8 @@ def errors(got, ref, norm):
 def make(name: str) -> str:
     import oracle
     from oracle.bf16_rows import bf16_rows_fwd_bwd
-    from bpt_inputs import WORKLOADS, make_inputs
-    w = WORKLOADS[name]
+    from bpt_inputs import make_inputs, workload
+    w = workload(name)
     t0 = time.time()
     inp = make_inputs(w, seed=SEED)
     p = oracle.params_from_inputs(inp)
@@ -97,7 +118,6 @@ def make(name: str) -> str:
         idx = rng.choice(v.size, size=min(NSAMPLE, v.size), replace=False)
         out[k + "_idx"] = idx.astype(np.int64)
         out[k + "_val"] = v.reshape(-1)[idx]
-        out[k + "_rms"] = np.float64(rms(v))
         out[k + "_shape"] = np.array(v.shape, dtype=np.int64)
     del g
     t1 = time.time()
@@ -116,5 +136,5 @@ def make(name: str) -> str:
 
 
 if __name__ == "__main__":
-    for n in sys.argv[1:] or ["bf16_7b_s32768", "bf16_rl_s96000", "bf16_13b_s65536"]:
+    for n in sys.argv[1:] or FULLSIZE:
         make(n)

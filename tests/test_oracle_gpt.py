@@ -143,3 +143,19 @@ def test_adamw_first_step_closed_form():
     np.testing.assert_allclose(pn, p - lr * wd * p - lr * g / (np.abs(g) + eps), rtol=1e-13, atol=1e-16)
     np.testing.assert_allclose(m, 0.1 * g, rtol=1e-15)
     np.testing.assert_allclose(v, 0.05 * g * g, rtol=1e-15)
+
+
+# ----------------------------------------------------------------------------- bf16 rounding model of the step
+def test_bf16_gpt_model_without_rounding_is_the_oracle():
+    """``oracle/bf16_gpt.py`` with its rounding off is the float64 GPT step; with it on
+    the loss moves by bf16-scale amounts only."""
+    from oracle.bf16_gpt import bf16_gpt_fwd_bwd
+    P, tok, tgt = tiny_model(5)
+    ref = gpt_fwd_bwd(tok, tgt, P, H)
+    m = bf16_gpt_fwd_bwd(tok, tgt, P, H, round_operands=False)
+    assert abs(m["loss"] - ref["loss"]) <= 1e-12 * abs(ref["loss"])
+    for name, _ in _entries(P):
+        np.testing.assert_allclose(_grad(m, name), _grad(ref, name), rtol=0, atol=1e-11, err_msg=name)
+    np.testing.assert_allclose(m["dX0"], ref["dX0"], rtol=0, atol=1e-11)
+    mr = bf16_gpt_fwd_bwd(tok, tgt, P, H)
+    assert 1e-6 < abs(mr["loss"] - ref["loss"]) / abs(ref["loss"]) < 2e-2
