@@ -59,7 +59,7 @@ def cpu_baseline(w, sample_S: int):
     return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"fwd+bwd of one sequence of {sample_S} tokens of the same layer shape "
                       f"(D={ws.D}, H={ws.H}, F={ws.F}, causal), float64 numpy, {dt:.1f} s",
-            "seconds": dt}
+            "seconds": dt, "host": host_cpu_info(threads)}
 
 
 # Sources whose every byte defines a launch class's kernel: a recorded HBM-traffic
@@ -116,6 +116,38 @@ def copy_probe(nbytes: int, reps: int) -> int:
     return 0
 
 
+def atomic_probe(steps: int) -> int:
+    """--atomic-probe: throughput of fp32 atomic adds into device memory, the cost of
+    accumulating dQ across key blocks in a fused attention backward. index_add_ along
+    dim 0 adds each row of src into the row of dst its index names with one fp32 atomic
+    add per element; rows of 8192 floats (32 KB, one 64 x 128 dQ tile), G source rows
+    onto `tiles` destination rows (several sources per destination: contention)."""
+    import torch
+    torch.cuda.set_device(0)
+    res = []
+    for tiles, G in ((4096, 4096), (512, 8192), (64, 8192)):
+        dst = torch.zeros(tiles, 8192, dtype=torch.float32, device="cuda")
+        src = torch.ones(G, 8192, dtype=torch.float32, device="cuda")
+        idx = torch.arange(G, device="cuda") % tiles
+        dst.index_add_(0, idx, src)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            dst.index_add_(0, idx, src)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        adds = G * 8192
+        res.append({"dst_rows": tiles, "src_rows": G, "ms": round(ms, 4), "gadds_per_s": round(adds / ms / 1e6, 1),
+                    "atomic_gb_per_s": round(4 * adds / ms / 1e6, 1)})
+        print(f"[atomic] {tiles} destination rows, {G} source rows: {ms:.3f} ms, "
+              f"{4 * adds / ms / 1e6:.0f} GB/s of fp32 atomic adds", file=sys.stderr, flush=True)
+    print(json.dumps({"atomic_probe": "torch index_add_ fp32 (global atomic add per element)", "points": res}),
+          flush=True)
+    return 0
+
+
 XENT_SHAPE = dict(T=32768, D=4096, V=50257)     # 7B-shaped tokens and width, GPT-2 vocabulary
 
 
@@ -139,7 +171,7 @@ def cpu_baseline_xent(D: int, V: int, ldw: int, sample_T: int):
     fl = 6.0 * sample_T * D * V
     return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"fwd+bwd of {sample_T} tokens of the same LM-head shape (D={D}, V={V}), "
-                      f"float64 numpy, {dt:.1f} s", "seconds": dt}
+                      f"float64 numpy, {dt:.1f} s", "seconds": dt, "host": host_cpu_info(threads)}
 
 
 def bench_xent(args) -> int:
@@ -259,7 +291,7 @@ def cpu_baseline_gpt(shape: dict, sample_L: int, sample_S: int):
             "sample": f"fwd+bwd (AdamW not timed) of {sample_L} of the {shape['L']} layers (D={D}, F={F}, H={H}) plus the "
                       f"V={V} head on one {sample_S}-token sequence, float64 numpy, {dt:.1f} s; its FLOP rate "
                       f"({fl / dt / 1e12:.3f} TFLOP/s) divided by the full model's FLOPs per token at "
-                      f"S={shape['S']}", "seconds": dt}
+                      f"S={shape['S']}", "seconds": dt, "host": host_cpu_info(threads)}
 
 
 def bench_gpt(args) -> int:
@@ -392,54 +424,59 @@ def gemm_yardstick(args) -> int:
     return 0
 
 
-def main() -> int:
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="bf16_7b_s32768")
-    ap.add_argument("--cpu-sample-s", type=int, default=4096)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
-                    help="only run a plain device copy of BYTES (counter calibration)")
-    ap.add_argument("--xent", action="store_true",
-                    help="measure the blockwise LM-head cross-entropy instead of the layer")
-    ap.add_argument("--gpt", action="store_true",
-                    help="measure a GPT-XL (1B) training step (24 layers, head, AdamW) instead of the layer")
-    ap.add_argument("--gpt-seq", type=int, default=0, help="sequence length of --gpt (default 16384)")
-    ap.add_argument("--gpt-batch", type=int, default=0, help="sequences per step of --gpt (default 1)")
-    ap.add_argument("--gemm-yardstick", action="store_true",
-                    help="time torch.matmul (hipBLASLt) on the 7B-shaped layer's GEMM shapes, then run the layer")
-    args = ap.parse_args()
-    if args.copy_probe:
-        return copy_probe(args.copy_probe, 3)
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
-              "sharding of the layer is a design, not part of this build", file=sys.stderr)
-        return 2
-    if args.xent:
-        return bench_xent(args)
-    if args.gpt:
-        return bench_gpt(args)
-    if args.gemm_yardstick:
-        rc = gemm_yardstick(args)
-        if rc:
-            return rc
+def host_cpu_info(threads: int) -> dict:
+    """The host CPU model and the BLAS library numpy's oracle runs on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = "unknown"
+    try:
+        from threadpoolctl import threadpool_info
+        libs = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if libs:
+            blas = f"{libs[0].get('internal_api')} {libs[0].get('version')}"
+    except Exception:  # pragma: no cover
+        pass
+    return {"cpu_model": model, "blas": blas, "threads": threads,
+            "cpus_available": len(os.sched_getaffinity(0))}
 
+
+def layer_buffers(w, cfg, bpt) -> dict:
+    """Bytes of every device buffer a fwd+bwd step holds (all allocated by the caller,
+    torch here; the library allocates nothing): the analytic peak HBM."""
+    E = 2 if w.dtype == "bf16" else 4
+    T, D, F = w.B * w.S, w.D, w.F
+    wts = (4 * D * D + 2 * D * F) * E
+    return {"weights": wts, "grads_fp32": (4 * D * D + 2 * D * F) * 4, "X_dY_Y_dX": 4 * T * D * E,
+            "saved": bpt.saved_bytes(cfg), "workspace_fwd": bpt.workspace_bytes(cfg, False),
+            "workspace_bwd": bpt.workspace_bytes(cfg, True)}
+
+
+def measure_layer(w, steps: int, warmup: int, verbose: bool = True) -> dict:
+    """Time `steps` fwd+bwd steps (after `warmup`) and `steps` forwards of workload w,
+    with the library's per-launch profiler on during the fwd+bwd steps; peak HBM over
+    the timed steps. Inputs are resident on the device before timing starts."""
     import torch
-    from bpt_inputs import WORKLOADS, make_inputs
+    from bpt_inputs import make_inputs
     from paper_2305_19370_amd import bpt
 
-    w = WORKLOADS[args.workload]
     dev = "cuda"
-    torch.cuda.set_device(0)
-    print(f"[bench] workload {w.name}: B={w.B} S={w.S} D={w.D} H={w.H} F={w.F} Bq={w.Bq} Bkv={w.Bkv} "
-          f"dtype={w.dtype}", file=sys.stderr, flush=True)
+    if verbose:
+        print(f"[bench] workload {w.name}: B={w.B} S={w.S} D={w.D} H={w.H} F={w.F} Bq={w.Bq} Bkv={w.Bkv} "
+              f"dtype={w.dtype}", file=sys.stderr, flush=True)
+    torch.cuda.empty_cache()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
     inp = make_inputs(w, seed=0)
     d = {k: (v.to(dev) if v is not None else None) for k, v in inp.items()}
     del inp
     cfg = bpt.make_config(w.B, w.S, w.D, w.H, w.F, w.Bq, w.Bkv, w.causal, w.dtype, w.dtype)
-    layer = bpt.Layer(cfg)
     wsf = torch.empty(bpt.workspace_bytes(cfg, False), dtype=torch.uint8, device=dev)
     wsb = torch.empty(bpt.workspace_bytes(cfg, True), dtype=torch.uint8, device=dev)
     out_dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
@@ -457,38 +494,139 @@ def main() -> int:
     def fwd():
         bpt.layer_fwd(cfg, d["X"], d, Y, saved, wsf)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    print(f"[bench] warmup done", file=sys.stderr, flush=True)
-
-    # forward alone
+    if verbose:
+        print(f"[bench] warmup done", file=sys.stderr, flush=True)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    for _ in range(args.steps):
+    for _ in range(steps):
         fwd()
     e1.record()
     torch.cuda.synchronize()
-    fwd_ms = e0.elapsed_time(e1) / args.steps
+    fwd_ms = e0.elapsed_time(e1) / steps
 
-    # timed fwd+bwd steps, with per-launch events from the library's profiler
-    torch.cuda.reset_peak_memory_stats()
     bpt.profile_enable(True)
     torch.cuda.synchronize()
     e0.record()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         step()
     e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     bpt.profile_enable(False)
     prof = bpt.profile_report()
-    ms = e0.elapsed_time(e1) / args.steps
-    peak_hbm = torch.cuda.max_memory_allocated()
+    ms = e0.elapsed_time(e1) / steps
+    peak = torch.cuda.max_memory_allocated() - base
     ok = bool(torch.isfinite(Y.float()).all() and torch.isfinite(dX.float()).all())
-    print(f"[bench] {args.steps} steps: {ms:.2f} ms/step (wall {wall / args.steps * 1e3:.2f}), fwd {fwd_ms:.2f} ms, "
-          f"finite={ok}", file=sys.stderr, flush=True)
+    bufs = layer_buffers(w, cfg, bpt)
+    group_rows = bpt.group_rows(cfg)
+    del d, wsf, wsb, Y, dX, saved, grads
+    torch.cuda.empty_cache()
+    if verbose:
+        print(f"[bench] {w.name} {steps} steps: {ms:.2f} ms/step (wall {wall / steps * 1e3:.2f}), fwd {fwd_ms:.2f} ms, "
+              f"peak {peak / 2 ** 30:.3f} GiB, finite={ok}", file=sys.stderr, flush=True)
+    return {"ms": ms, "fwd_ms": fwd_ms, "peak": peak, "buffers": bufs, "prof": prof, "ok": ok,
+            "group_rows": group_rows}
+
+
+def linear_fit(xs, ys):
+    """Least-squares y = a + b x; returns (a, b, R^2)."""
+    n = len(xs)
+    mx, my = sum(xs) / n, sum(ys) / n
+    sxx = sum((x - mx) ** 2 for x in xs)
+    sxy = sum((x - mx) * (y - my) for x, y in zip(xs, ys))
+    b = sxy / sxx
+    a = my - b * mx
+    ss_res = sum((y - a - b * x) ** 2 for x, y in zip(xs, ys))
+    ss_tot = sum((y - my) ** 2 for y in ys)
+    return a, b, 1.0 - ss_res / ss_tot if ss_tot > 0 else 1.0
+
+
+def bench_sweep(args) -> int:
+    """--sweep-s: the 13B-shaped layer at each sequence length of the list: fwd and
+    fwd+bwd TFLOP/s, tokens/s, peak HBM against the analytic sum of the step's buffers,
+    and a linear fit of peak HBM in S."""
+    import torch
+    from bpt_inputs import sweep_workload
+    torch.cuda.set_device(0)
+    pts = []
+    for S in [int(x) for x in args.sweep_s.split(",")]:
+        w = sweep_workload(S)
+        r = measure_layer(w, args.steps, args.warmup)
+        ffwd = model_flops_fwd(w.B, w.S, w.D, w.F, w.causal)
+        expected = sum(r["buffers"].values())
+        pts.append({"S": S, "ms_per_step": round(r["ms"], 3), "fwd_ms": round(r["fwd_ms"], 3),
+                    "tflops": round(3 * ffwd / (r["ms"] / 1e3) / 1e12, 1),
+                    "fwd_tflops": round(ffwd / (r["fwd_ms"] / 1e3) / 1e12, 1),
+                    "tokens_per_s": round(w.B * S / (r["ms"] / 1e3), 1),
+                    "peak_hbm_bytes": int(r["peak"]), "expected_bytes": int(expected),
+                    "buffers": r["buffers"], "group_rows": r["group_rows"],
+                    "avoided_scores_bytes": 2 * w.B * w.H * S * S,          # one [B, H, S, S] bf16
+                    "avoided_ffn_bytes": 2 * w.B * S * w.F, "finite": r["ok"]})
+        del r
+    a, b, r2 = linear_fit([p["S"] for p in pts], [p["peak_hbm_bytes"] for p in pts])
+    out = {"metric": "BPT layer fwd+bwd TFLOP/s, tokens/s and peak HBM against sequence length (13B-shaped)",
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": "bf16_13b_sweep", "B": 1, "D": 5120, "H": 40, "F": 20480, "Bq": 2048,
+                      "Bkv": 2048, "causal": True},
+           "points": pts,
+           "peak_hbm_fit": {"intercept_bytes": a, "bytes_per_token": b, "r2": r2}}
+    print(json.dumps(out), flush=True)
+    return 0 if all(p["finite"] for p in pts) else 1
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="bf16_7b_s32768")
+    ap.add_argument("--cpu-sample-s", type=int, default=4096)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES (counter calibration)")
+    ap.add_argument("--xent", action="store_true",
+                    help="measure the blockwise LM-head cross-entropy instead of the layer")
+    ap.add_argument("--gpt", action="store_true",
+                    help="measure a GPT-XL (1B) training step (24 layers, head, AdamW) instead of the layer")
+    ap.add_argument("--gpt-seq", type=int, default=0, help="sequence length of --gpt (default 16384)")
+    ap.add_argument("--gpt-batch", type=int, default=0, help="sequences per step of --gpt (default 1)")
+    ap.add_argument("--atomic-probe", action="store_true",
+                    help="only measure the throughput of fp32 atomic adds into device memory")
+    ap.add_argument("--sweep-s", default="", metavar="S1,S2,...",
+                    help="measure the 13B-shaped layer at each of these sequence lengths (peak HBM vs S)")
+    ap.add_argument("--gemm-yardstick", action="store_true",
+                    help="time torch.matmul (hipBLASLt) on the 7B-shaped layer's GEMM shapes, then run the layer")
+    args = ap.parse_args()
+    if args.copy_probe:
+        return copy_probe(args.copy_probe, 3)
+    if args.atomic_probe:
+        return atomic_probe(args.steps)
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
+              "sharding of the layer is a design, not part of this build", file=sys.stderr)
+        return 2
+    if args.xent:
+        return bench_xent(args)
+    if args.gpt:
+        return bench_gpt(args)
+    if args.sweep_s:
+        return bench_sweep(args)
+    if args.gemm_yardstick:
+        rc = gemm_yardstick(args)
+        if rc:
+            return rc
+
+    import torch
+    from bpt_inputs import workload
+
+    w = workload(args.workload)
+    torch.cuda.set_device(0)
+    r = measure_layer(w, args.steps, args.warmup)
+    ms, fwd_ms, prof, ok, peak_hbm = r["ms"], r["fwd_ms"], r["prof"], r["ok"], r["peak"]
 
     ffwd = model_flops_fwd(w.B, w.S, w.D, w.F, w.causal)
     value = 3 * ffwd / (ms / 1e3) / 1e12
@@ -526,12 +664,13 @@ def main() -> int:
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "S": w.S, "D": w.D, "H": w.H, "F": w.F, "Bq": w.Bq,
-                   "Bkv": w.Bkv, "causal": w.causal, "group_rows": bpt.group_rows(cfg)},
+                   "Bkv": w.Bkv, "causal": w.causal, "group_rows": r["group_rows"]},
         "pct_of_peak": round(100 * value / peak, 2),
         "tokens_per_s": round(w.B * w.S / (ms / 1e3), 1),
         "fwd_ms": round(fwd_ms, 3),
         "fwd_tflops": round(ffwd / (fwd_ms / 1e3) / 1e12, 2),
         "peak_hbm_gib": round(peak_hbm / 2 ** 30, 3),
+        "expected_hbm_gib": round(sum(r["buffers"].values()) / 2 ** 30, 3),
         "roofline": roof,
         "kernels": breakdown,
     }

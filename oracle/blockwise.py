@@ -1,17 +1,25 @@
 """Algorithm 1 of the paper in float64 — TEST INFRASTRUCTURE (see ``oracle/__init__.py``).
 
-For each query block (rows [i*Bq, min((i+1)*Bq, S)) of one sequence), iterate
-over the key/value blocks (rows [j*Bkv, ...)), keep per query row a running
-maximum, a running numerator and a running denominator, and rescale them by
-exp(old_max - new_max) whenever the maximum grows (the carry update of
-Section 3 and Fig. 3: numerator * correction + exp(scores - max) V, likewise
-for the denominator). Once every key/value block has been visited the block's
-attention is numerator / denominator, after which the output projection, the
-FFN and both residuals are applied to that query block before the next query
-block starts (Algorithm 1, last two steps of the outer loop).
+Attention of a query block is assembled from its key/value blocks the way Section 3
+combines blocks (eq. 3 and the rescaling that follows it): each key/value block j
+on its own yields, per query row, a summary triple
 
-Bq and Bkv are block LENGTHS in tokens and need not divide S: the last block
-of a sequence is shorter. Blocks are contiguous token ranges.
+    m_j = max_k s_k,   l_j = sum_k exp(s_k - m_j),   a_j = sum_k exp(s_k - m_j) v_k
+
+over its keys k (s the scaled scores), and two summaries merge exactly into the
+summary of their union by bringing both to the larger maximum:
+
+    m = max(m_1, m_2),   l = l_1 e^(m_1 - m) + l_2 e^(m_2 - m),   a = a_1 e^(m_1 - m) + a_2 e^(m_2 - m).
+
+Folding the blocks in key order and reading out a / l gives the query block's
+attention, and m + log l its log-sum-exp. Then the output projection, the FFN and
+both residuals are applied to that query block before the next one starts
+(Algorithm 1's outer loop).
+
+Bq and Bkv are block LENGTHS in tokens and need not divide S: the last block of a
+sequence is shorter. Blocks are contiguous token ranges. A row whose keys in a
+block are all masked has the empty summary (m = -inf, l = 0, a = 0), which the
+merge leaves unchanged.
 
 This is a second, independently structured route to the same numbers as
 ``oracle.layer``; the tests require the two to agree to ~1e-12 for many
@@ -26,33 +34,36 @@ import numpy as np
 from .layer import LayerParams, act_fwd, layer_norm_fwd
 
 
-def _attend_query_block(q_scaled, K, V, rows, causal, Bkv):
-    """Online-softmax attention of one query block against all key/value blocks.
+def _block_summary(s, v):
+    """(m, l, a) of one key/value block for every query row; s [nq, nk] scaled scores
+    (-inf where masked), v [nk, dh]."""
+    m = s.max(axis=1)
+    e = np.exp(s - np.where(np.isfinite(m), m, 0.0)[:, None])     # 0 wherever s = -inf
+    return m, e.sum(axis=1), e @ v
 
-    q_scaled: [nq, dh] queries already divided by sqrt(dh) (the listing scales
-    the query once up front). rows: absolute positions of the queries.
-    Returns (attention [nq, dh], log-sum-exp [nq])."""
+
+def _merge(x, y):
+    """Summary of the union of two disjoint key sets from their summaries."""
+    (m1, l1, a1), (m2, l2, a2) = x, y
+    m = np.maximum(m1, m2)
+    ref = np.where(np.isfinite(m), m, 0.0)
+    c1, c2 = np.exp(m1 - ref), np.exp(m2 - ref)                     # exp(-inf) = 0 for empty ones
+    return m, l1 * c1 + l2 * c2, a1 * c1[:, None] + a2 * c2[:, None]
+
+
+def _attend_query_block(q_scaled, K, V, rows, causal, Bkv):
+    """Attention of one query block (queries already divided by sqrt(dh); rows their
+    absolute positions) against every key/value block. Returns (O [nq, dh], lse [nq])."""
     nq, dh = q_scaled.shape
-    S_kv = K.shape[0]
-    numerator = np.zeros((nq, dh))
-    denominator = np.zeros(nq)
-    running_max = np.full(nq, -np.inf)
-    for k0 in range(0, S_kv, Bkv):
-        k1 = min(k0 + Bkv, S_kv)
-        scores = q_scaled @ K[k0:k1].T                       # scores of this block pair
+    acc = (np.full(nq, -np.inf), np.zeros(nq), np.zeros((nq, dh)))   # the empty summary
+    for k0 in range(0, K.shape[0], Bkv):
+        k1 = min(k0 + Bkv, K.shape[0])
+        s = q_scaled @ K[k0:k1].T
         if causal:
-            keys = np.arange(k0, k1)
-            scores = np.where(keys[None, :] <= rows[:, None], scores, -np.inf)
-        new_max = np.maximum(running_max, scores.max(axis=1))
-        # A row that has seen only masked keys so far keeps max = -inf; its weights
-        # and its correction are exactly 0 (avoids -inf - -inf).
-        ref = np.where(np.isfinite(new_max), new_max, 0.0)
-        weights = np.exp(scores - ref[:, None])
-        correction = np.exp(running_max - ref)
-        numerator = numerator * correction[:, None] + weights @ V[k0:k1]
-        denominator = denominator * correction + weights.sum(axis=1)
-        running_max = new_max
-    return numerator / denominator[:, None], running_max + np.log(denominator)
+            s = np.where(np.arange(k0, k1)[None, :] <= rows[:, None], s, -np.inf)
+        acc = _merge(acc, _block_summary(s, V[k0:k1]))
+    m, l, a = acc
+    return a / l[:, None], m + np.log(l)
 
 
 def blockwise_attention_head(Q, K, V, causal: bool, Bq: int, Bkv: int):

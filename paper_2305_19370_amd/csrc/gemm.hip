@@ -7,10 +7,11 @@
 // feature-major gradients contracted over features), which the kernel transposes
 // on its way from LDS into the MFMA registers.
 //
-// bf16 path: gfx950 MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation, 256 threads
-// (2 x 2 waves), K step 32 per stage through an LDS ring with XOR-swizzled 16-byte
-// chunks, so that the rows a fragment read touches fall in distinct banks. fp32 path:
-// plain VALU FMA tiles (used for the fp32 parity workload).
+// bf16 path: gfx950 MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation; tiles of 256 x 256
+// with 8 waves (2 along M x 4 along N, two per SIMD) or, where fewer than 256 such tiles
+// exist, 128 x 128 with 4 waves (2 x 2); K step 32 per stage through an LDS ring with
+// XOR-swizzled 16-byte chunks, so that the rows a fragment read touches fall in distinct
+// banks. fp32 path: plain VALU FMA tiles (used for the fp32 parity workload).
 #include "common.h"
 #include "internal.h"
 #include <type_traits>
@@ -192,7 +193,7 @@ BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const
 }
 
 // ------------------------------------------------------------------ bf16 MFMA kernel
-// Tile BM x BN (2 x 2 waves), K step 32 per stage, NS stages in an LDS ring filled
+// Tile BM x BN (2 x NWN waves), K step 32 per stage, NS stages in an LDS ring filled
 // by direct global->LDS copies (global_load_lds_dwordx4) issued NS-1 stages ahead.
 // Tile rows are 32 bf16 (64 bytes, four 16-byte chunks) stored unpadded; chunk c of
 // row r sits at chunk position c ^ swz(r), which spreads the rows that one fragment read
