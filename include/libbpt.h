@@ -69,8 +69,10 @@ typedef struct {
   int32_t causal;          /* 1: query q sees key k iff k <= q, within one sequence        */
   int32_t dtype;           /* bpt_dtype of X, dY, weights and saved activations             */
   int32_t out_dtype;       /* bpt_dtype of Y and dX                                         */
-  int32_t group_blocks;    /* query blocks per FFN group (rows of the [., F] intermediate   */
-                           /* live at once = group_blocks * Bq); 0 = automatic              */
+  int32_t group_blocks;    /* query blocks per FFN group: at most group_blocks * Bq rows of */
+                           /* the [., F] intermediate are live at once (a run of one         */
+                           /* sequence, or several whole sequences when two or more fit);    */
+                           /* 0 = automatic (8192 rows)                                      */
   float ln_eps;            /* LayerNorm epsilon (biased variance), e.g. 1e-5                */
   int32_t activation;      /* bpt_activation of the FFN                                     */
   float dropout;           /* rate p in [0, 1) of dropout on the two residual branches:     */
@@ -116,8 +118,9 @@ typedef struct {
 /* Host-only checks of a configuration; never touches a GPU. */
 bpt_status bpt_validate(const bpt_config* cfg);
 
-/* Rows of the [., F] FFN intermediate that are live at once (group_blocks * Bq,
- * clipped to S). Returns -1 for an invalid configuration. Host-only. */
+/* Rows of the [., F] FFN intermediate that are live at once: group_blocks * Bq clipped to
+ * S, or, when that holds two or more whole sequences, the most whole sequences it holds
+ * (at most B) times S. Returns -1 for an invalid configuration. Host-only. */
 int64_t bpt_group_rows(const bpt_config* cfg);
 
 /* Size of the `saved` buffer and the offsets inside it. Section 3.1's memory analysis
@@ -209,8 +212,9 @@ typedef struct {
 bpt_status bpt_xent_validate(const bpt_xent_config* cfg);
 
 /* Workspace of bpt_xent_fwd (backward = 0): block_rows * ldw fp32 logits + T floats;
- * of bpt_xent_bwd (backward = 1): block_rows (rounded up to 64) * ldw elements of
- * cfg->dtype. Returns 0 for an invalid configuration. Host-only. */
+ * of bpt_xent_bwd (backward = 1): ldw * block_rows (rounded up to 64) elements of
+ * cfg->dtype (one block's logit gradient, vocabulary-major). Returns 0 for an invalid
+ * configuration. Host-only. */
 size_t bpt_xent_workspace_bytes(const bpt_xent_config* cfg, int backward);
 
 /* Forward. targets: [T] int32 class indices; a target outside [0, V) makes that

@@ -51,6 +51,18 @@ BPT_DEV float xent_grad(const GemmArgs& a, int64_t n, float v, float lse, int y)
   const float p = __builtin_amdgcn_exp2f((v - lse) * 1.4426950408889634f);
   return a.alpha * (n == y ? p - 1.0f : p);
 }
+// EPI_XENT_T: the same for element (m, n) of the transposed logits, vocabulary index m
+// and token n. Edge tiles and full tiles (whose epilogue holds each column's base-2
+// log-sum-exp) evaluate the same expression, so a token's gradient does not depend on
+// where the tile boundaries fall.
+BPT_DEV float xent_grad_t_l2(const GemmArgs& a, int64_t m, float v, float lse2, int y) {
+  if (m >= a.nvalid) return 0.0f;
+  const float p = __builtin_amdgcn_exp2f(fmaf(v, 1.4426950408889634f, -lse2));
+  return a.alpha * (m == y ? p - 1.0f : p);
+}
+BPT_DEV float xent_grad_t(const GemmArgs& a, int64_t m, int64_t n, float v) {
+  return xent_grad_t_l2(a, m, v, a.rowv[n] * 1.4426950408889634f, a.tgt[n]);
+}
 
 template <int EPI, typename CT, typename RT>
 BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float v) {
@@ -80,6 +92,8 @@ BPT_DEV void epi_store(const GemmArgs& a, int64_t z, int64_t m, int64_t n, float
     if (a.C2) c2_store(a, z * a.sC2 + m * a.ldc2 + n, gp);
   } else if constexpr (EPI == EPI_XENT) {
     C[idx] = from_f32<CT>(xent_grad(a, n, v, a.rowv[m], a.tgt[m]));
+  } else if constexpr (EPI == EPI_XENT_T) {
+    C[idx] = from_f32<CT>(xent_grad_t(a, m, n, v));
   } else {  // EPI_MUL
     const RT* R = (const RT*)a.R + z * a.sR;
     C[idx] = from_f32<CT>(v * to_f32<RT>(R[m * a.ldr + n]));
@@ -147,6 +161,9 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
     const int y = a.tgt[m];
 #pragma unroll
     for (int e = 0; e < 4; ++e) v[e] = xent_grad(a, n + e, v[e], lse, y);
+  } else if constexpr (EPI == EPI_XENT_T) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = xent_grad_t(a, m, n + e, v[e]);
   } else {
     v *= V4<RT>::ld((const RT*)a.R + z * a.sR + m * a.ldr + n);
   }
@@ -157,10 +174,11 @@ BPT_DEV void epi_store4(const GemmArgs& a, int64_t z, int64_t m, int64_t n, int6
 // already at (m, n): c into C, r into R (EPI_RESID / EPI_MUL; for an fp32 C that
 // accumulates, the values of C already loaded); c2 is the element index of (m, n) in
 // C2 (EPI_GELU / EPI_RELU); bn at bias[n]; bm = bias[m] for a per-row bias, or the row's
-// log-sum-exp for EPI_XENT, whose column is n and target y.
+// log-sum-exp for EPI_XENT, whose column is n and target y; EPI_XENT_T takes row m
+// (passed as y) and column n.
 template <int EPI, typename CT, typename RT>
 BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const float* bn, float bm, f32x4 v,
-                      int64_t n = 0, int y = 0) {
+                      int64_t n = 0, int64_t y = 0) {
   if constexpr (EPI == EPI_STORE) {
     v *= a.alpha;
     if constexpr (sizeof(CT) == 4) {
@@ -185,7 +203,10 @@ BPT_DEV void epi_vec4(const GemmArgs& a, CT* c, const void* r, int64_t c2, const
     if (a.C2) c2_store4(a, c2, d);
   } else if constexpr (EPI == EPI_XENT) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = xent_grad(a, n + e, v[e], bm, y);
+    for (int e = 0; e < 4; ++e) v[e] = xent_grad(a, n + e, v[e], bm, (int)y);
+  } else if constexpr (EPI == EPI_XENT_T) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = xent_grad_t(a, y, n + e, v[e]);
   } else {
     v *= V4<RT>::ld((const RT*)r);
   }
@@ -546,15 +567,38 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
       constexpr int RS = (int)sizeof(RT);
       // the GELU epilogue is long: keep its loop rolled (instruction cache)
       constexpr int UNR = kAct<EPI> ? 4 : 32 / RSTEP;
+      if constexpr (EPI == EPI_XENT_T) {
+        // a lane's four columns (tokens) are the same on every row of the strip: their
+        // log-sum-exp (base 2) and targets are loaded once
+        float l2[4];
+        int y4[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          l2[e] = a.rowv[ncol + c0 + e] * 1.4426950408889634f;
+          y4[e] = a.tgt[ncol + c0 + e];
+        }
+#pragma unroll 4
+        for (int it = 0; it < 32 / RSTEP; ++it) {
+          const int row = r0 + RSTEP * it;
+          const int64_t m = mrow + row;                // vocabulary index
+          f32x4 v = *(const f32x4*)(strip + row * PITCHF + c0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = xent_grad_t_l2(a, m, v[e], l2[e], y4[e]);
+          V4<CT>::st(cb + (int64_t)RSTEP * it * a.ldc, v);
+        }
+        continue;
+      }
 #pragma unroll UNR
       for (int it = 0; it < 32 / RSTEP; ++it) {
         const int row = r0 + RSTEP * it;
         const f32x4 v = *(const f32x4*)(strip + row * PITCHF + c0);
         float bm = (kAct<EPI> && a.bias && a.bias_on_m) ? a.bias[mrow + row] : 0.0f;
-        int y = 0;
+        int64_t y = 0;
         if constexpr (EPI == EPI_XENT) {
           bm = a.rowv[mrow + row];
           y = a.tgt[mrow + row];
+        } else if constexpr (EPI == EPI_XENT_T) {
+          y = mrow + row;                              // the row's vocabulary index
         }
         if constexpr (PRE)
           epi_vec4<EPI, CT, RT>(a, cb + (int64_t)RSTEP * it * a.ldc, &pre[i % PD][it], 0, bb, bm, v);
@@ -673,7 +717,7 @@ static hipError_t launch_typed(Dt ab, const GemmArgs& a, hipStream_t s) {
       return hipErrorInvalidValue;
     }
     if (a.trans_a) {
-      if constexpr (EPI == EPI_STORE || kAct<EPI>)
+      if constexpr (EPI == EPI_STORE || kAct<EPI> || EPI == EPI_XENT_T)
         return big >= 256 ? launch_bf16<256, 256, EPI, CT, RT, true, false, kNWN>(a, s)
                           : launch_bf16<128, 128, EPI, CT, RT, true, false>(a, s);
       return hipErrorInvalidValue;
@@ -699,6 +743,9 @@ hipError_t gemm(Dt ab, Epi epi, Dt ct, Dt rt, const GemmArgs& a, hipStream_t s) 
     case EPI_XENT:
       return ct == F32 ? launch_typed<EPI_XENT, float, float>(ab, a, s)
                        : launch_typed<EPI_XENT, bf16, float>(ab, a, s);
+    case EPI_XENT_T:
+      return ct == F32 ? launch_typed<EPI_XENT_T, float, float>(ab, a, s)
+                       : launch_typed<EPI_XENT_T, bf16, float>(ab, a, s);
     case EPI_MUL:
       if (rt == F16)
         return ct == F32 ? launch_typed<EPI_MUL, float, f16>(ab, a, s)

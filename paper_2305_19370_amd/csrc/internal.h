@@ -21,6 +21,9 @@ enum Epi {
                    // C = alpha (exp(acc - rowv[m]) - [n == tgt[m]]), rowv the row's
                    // log-sum-exp; C = 0 for nvalid <= n
   EPI_RELU = 5,    // as EPI_GELU with max(0, z) and its derivative (0 at z = 0)
+  EPI_XENT_T = 6,  // EPI_XENT on the transposed logits (rows m = vocabulary, columns n =
+                   // tokens): for m < nvalid C = alpha (exp(acc - rowv[n]) - [m == tgt[n]]),
+                   // C = 0 for nvalid <= m
 };
 
 struct GemmArgs {
@@ -39,12 +42,12 @@ struct GemmArgs {
   int accumulate = 0;          // fp32 C only: C += acc
   float alpha = 1.0f;          // EPI_STORE: acc is multiplied by alpha before it is stored;
                                // EPI_XENT: the gradient's scale
-  const float* rowv = nullptr; // EPI_XENT: per-row log-sum-exp (natural log), [M]
-  const int32_t* tgt = nullptr;// EPI_XENT: per-row target column, [M]
-  int64_t nvalid = 0;          // EPI_XENT: columns from nvalid on are not logits
+  const float* rowv = nullptr; // EPI_XENT: per-row log-sum-exp (natural log), [M]; EPI_XENT_T: per column, [N]
+  const int32_t* tgt = nullptr;// EPI_XENT: per-row target column, [M]; EPI_XENT_T: per-column target row, [N]
+  int64_t nvalid = 0;          // EPI_XENT: columns from nvalid on are not logits; EPI_XENT_T: rows
   int bias_on_m = 0;           // EPI_GELU / EPI_RELU: bias indexed by row instead of column
-  // Transposed operands (trans_b with any epilogue, trans_a with EPI_STORE, EPI_GELU or EPI_RELU,
-  // both with EPI_STORE): trans_a means A is stored K-major, element
+  // Transposed operands (trans_b with any epilogue, trans_a with EPI_STORE, EPI_GELU, EPI_RELU or
+  // EPI_XENT_T, both with EPI_STORE): trans_a means A is stored K-major, element
   // (m, k) at A[k * lda + m]; likewise trans_b for B (element (n, k) at B[k * ldb + n]).
   // For such an operand, x_rows is the number of k rows that may be read (rows from
   // x_rows up to K are not read, and the other operand must be zero at those k), and

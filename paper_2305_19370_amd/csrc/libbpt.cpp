@@ -40,6 +40,7 @@ size_t esize(int32_t dt) { return dt == BPT_BF16 ? 2 : 4; }
 
 struct Dims {
   int64_t B, S, D, H, F, dh, T, Sp, Tp, R, Rp;
+  int64_t nbg, Rs;       // FFN group: nbg whole sequences (Rs = S), or Rs rows of one (nbg = 1)
   size_t E;
   bool drop;             // residual-branch dropout on (rate > 0)
 };
@@ -54,7 +55,18 @@ Dims dims_of(const bpt_config& c) {
   d.Tp = c.B * d.Sp;
   const int64_t g = c.group_blocks > 0 ? c.group_blocks
                                       : std::max<int64_t>(1, (kDefaultGroupRows + c.Bq - 1) / c.Bq);
-  d.R = std::min<int64_t>(g * c.Bq, c.S);
+  // A group holds up to g * Bq rows: a run of Rs rows of one sequence or, when at least two
+  // whole sequences fit, nbg whole sequences (their tokens are contiguous), so that short
+  // sequences still give the FFN GEMMs their full height.
+  const int64_t rows = g * c.Bq;
+  if (c.B > 1 && rows >= 2 * c.S) {
+    d.nbg = std::min<int64_t>(c.B, rows / c.S);
+    d.Rs = c.S;
+  } else {
+    d.nbg = 1;
+    d.Rs = std::min<int64_t>(rows, c.S);
+  }
+  d.R = d.nbg * d.Rs;
   d.Rp = rup(d.R, 64);
   d.E = esize(c.dtype);
   return d;
@@ -304,7 +316,7 @@ XentDims xent_dims(const bpt_xent_config& c) {
 struct XentWs {
   float* logits;   // forward: [R, ldw] fp32
   float* tok;      // forward: [T] token losses
-  void* g;         // backward: [Rp, ldw] in dtype, the logits' gradient of one block
+  void* g;         // backward: [ldw, Rp] in dtype, the logits' gradient of one block, transposed
 };
 
 XentWs xent_ws(const XentDims& d, void* base, int backward, int64_t* total) {
@@ -398,13 +410,15 @@ size_t bpt_describe(const bpt_config* cfg, char* buf, size_t n) {
   const bool bf = cfg->dtype == BPT_BF16;
   int w = snprintf(buf, n,
                    "dtype=%s attention: q-tile=%d kv-step=%d (%s); backward dK/dV kv-tile=%d q-step=%d, "
-                   "dQ q-tile=%d kv-step=%d; gemm: %s; ffn %s, group rows=%lld (%lld query blocks of %lld)",
+                   "dQ q-tile=%d kv-step=%d; gemm: %s; ffn %s, group rows=%lld (%lld sequence(s) x %lld rows; "
+                   "query blocks of %lld)",
                    bf ? "bf16" : "f32", bf ? 256 : 64, bf ? 64 : 32,
                    bf ? "MFMA 32x32x16 bf16, fp32 accumulate, 32 rows per wave" : "fp32 VALU",
                    bf ? 256 : 64, bf ? 64 : 16, bf ? 256 : 64, bf ? 64 : 16,
                    bf ? "MFMA bf16 256x256 (8 waves) or 128x128 (4 waves) tiles, K-step 32"
                       : "fp32 VALU 64x64 tiles",
-                   cfg->activation == BPT_RELU ? "relu" : "gelu", (long long)d.R, (long long)((d.R + cfg->Bq - 1) / cfg->Bq), (long long)cfg->Bq);
+                   cfg->activation == BPT_RELU ? "relu" : "gelu", (long long)d.R, (long long)d.nbg, (long long)d.Rs,
+                   (long long)cfg->Bq);
   return w < 0 ? 0 : std::min((size_t)w, n - 1);
 }
 
@@ -491,9 +505,10 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
 
   // Outer loop over groups of query blocks: attention for the group, then the
   // output projection, LN2, FFN and both residuals for the same rows.
-  for (int64_t b = 0; b < d.B; ++b) {
-    for (int64_t s0 = 0; s0 < d.S; s0 += d.R) {
-      const int64_t r = std::min(d.R, d.S - s0);
+  for (int64_t b = 0; b < d.B; b += d.nbg) {
+    const int64_t nb = std::min(d.nbg, d.B - b);   // sequences in this group (several only if whole)
+    for (int64_t s0 = 0; s0 < d.S; s0 += d.Rs) {
+      const int64_t rs = std::min(d.Rs, d.S - s0), r = nb * rs;
       const int64_t t0 = b * d.S + s0;
       AttnArgs a;
       a.q = sv.qkv; a.ld_q = 3 * D;
@@ -502,9 +517,9 @@ bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params*
       a.o = sv.o; a.ld_o = D;
       a.lse = sv.lse;
       a.S = d.S; a.Sp = d.Sp; a.B = (int)d.B; a.H = (int)d.H; a.dh = (int)d.dh; a.causal = cfg->causal;
-      a.q_begin = s0; a.q_end = s0 + r; a.b_begin = (int)b; a.nb = 1;
-      const double pairs = attn_pairs(s0, s0 + r, d.S, cfg->causal) * d.H;
-      RUN("attn.fwd", 4.0 * d.dh * pairs, (3.0 * r + 2.0 * (s0 + r)) * D * E_, attn_fwd(E, a, s));
+      a.q_begin = s0; a.q_end = s0 + rs; a.b_begin = (int)b; a.nb = (int)nb;
+      const double pairs = attn_pairs(s0, s0 + rs, d.S, cfg->causal) * d.H * nb;
+      RUN("attn.fwd", 4.0 * d.dh * pairs, (3.0 * rs + 2.0 * (s0 + rs)) * nb * D * E_, attn_fwd(E, a, s));
 
       GemmArgs go;     // h = X + O Wo
       go.A = off(sv.o, t0 * D * E_); go.lda = D; go.B = p->Wo; go.ldb = D; go.trans_b = 1;
@@ -594,9 +609,10 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
     RUN("dropout.bwd", 0, (double)T * D * 2 * E_, dropout_scale(E, dY, E, w.dYm, T, D, drop_args(*cfg, 1, 0), s));
     dYf = w.dYm;
   }
-  for (int64_t b = 0; b < d.B; ++b) {
-    for (int64_t s0 = 0; s0 < S; s0 += d.R) {
-      const int64_t r = std::min(d.R, S - s0), rp = rup(r, 64), t0 = b * S + s0;
+  for (int64_t b = 0; b < d.B; b += d.nbg) {
+    const int64_t nb = std::min(d.nbg, d.B - b);
+    for (int64_t s0 = 0; s0 < S; s0 += d.Rs) {
+      const int64_t r = nb * std::min(d.Rs, S - s0), rp = rup(r, 64), t0 = b * S + s0;
       const void* dYg = off(dYf, t0 * D * E_);
       RUN("layernorm.fwd", 0, (double)r * D * (4 + E_),
           layer_norm(F32, E, sv.h + t0 * D, D, p->ln2_g, p->ln2_b, w.vg, D, sv.mu2 + t0, sv.rstd2 + t0, r, D,
@@ -811,29 +827,30 @@ bpt_status bpt_xent_bwd(const bpt_xent_config* cfg, const void* h, const void* W
   const Dt E = cfg->dtype == BPT_BF16 ? BF16 : F32;
   const int64_t E_ = (int64_t)d.E;
   for (int64_t t0 = 0; t0 < d.T; t0 += d.R) {
-    const int64_t r = std::min(d.R, d.T - t0), rk = rup(r, 32);
+    const int64_t r = std::min(d.R, d.T - t0), rp = rup(r, 64);
     const char* hb = (const char*)h + t0 * d.D * E_;
-    {   // G = (dloss / T)(softmax - onehot) of the block's logits, recomputed
+    {   // G^T [ldw, rp] = (dloss / T)(softmax - onehot) of the block's logits, recomputed
+        // transposed (W read as stored is the K-major A operand, h the contiguous B);
+        // columns past r and rows past V are written as zeros
       GemmArgs g;
-      g.A = hb; g.lda = d.D; g.B = W; g.ldb = d.ldw; g.trans_b = 1;
-      g.C = w.g; g.ldc = d.ldw; g.M = r; g.N = d.ldw; g.K = d.D;
+      g.A = W; g.lda = d.ldw; g.trans_a = 1; g.B = hb; g.ldb = d.D;
+      g.C = w.g; g.ldc = d.Rp; g.M = d.ldw; g.N = r; g.Nstore = rp; g.K = d.D;
       g.alpha = dloss / (float)d.T; g.rowv = lse + t0; g.tgt = targets + t0; g.nvalid = d.V;
-      RUN("xent.grad_logits", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_XENT, E, F32, g, s));
+      RUN("xent.grad_logits", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_XENT_T, E, F32, g, s));
     }
-    if (rk > r)   // the product over tokens below reads rk rows of G: zero the pad rows
-      RUN("xent.fill", 0, (double)(rk - r) * d.ldw * E_,
-          fill_zero((char*)w.g + r * d.ldw * E_, (rk - r) * d.ldw * E_, s));
-    {   // dh = G W^T (W rows are contiguous along the vocabulary: the plain NT form)
+    {   // dh = G W^T: G read from its transposed copy (K-major A), W rows contiguous along
+        // the vocabulary
       GemmArgs g;
-      g.A = w.g; g.lda = d.ldw; g.B = W; g.ldb = d.ldw;
+      g.A = w.g; g.lda = d.Rp; g.trans_a = 1; g.a_cols = d.Rp; g.B = W; g.ldb = d.ldw;
       g.C = (char*)dh + t0 * d.D * E_; g.ldc = d.D; g.M = r; g.N = d.D; g.K = d.ldw;
       RUN("xent.dh", gemm_flops(g), gemm_bytes(g, E_, E_), gemm(E, EPI_STORE, E, F32, g, s));
     }
-    if (dW) {   // dW = h^T G: h and G both read token-major (G is zero past row r)
+    if (dW) {   // dW = h^T G: h read token-major (K-major A), G^T rows contiguous along the
+                // tokens (zero past row r)
       GemmArgs g;
       g.A = hb; g.lda = d.D; g.trans_a = 1; g.a_rows = r;
-      g.B = w.g; g.ldb = d.ldw; g.trans_b = 1; g.b_rows = rk;
-      g.C = dW; g.ldc = d.ldw; g.M = d.D; g.N = d.ldw; g.K = rk; g.accumulate = t0 > 0;
+      g.B = w.g; g.ldb = d.Rp;
+      g.C = dW; g.ldc = d.ldw; g.M = d.D; g.N = d.ldw; g.K = rp; g.accumulate = t0 > 0;
       RUN("xent.dW", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
     }
   }

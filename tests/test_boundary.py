@@ -145,6 +145,22 @@ def test_group_rows_and_describe():
     assert big - small >= 7 * 1024 * 16384 * 2
 
 
+def test_groups_of_whole_sequences():
+    """A group holds several whole sequences when at least two fit in group_blocks * Bq
+    rows (and never more sequences than the batch has); otherwise a run of one."""
+    c = bpt.make_config(2, 4096, 2048, 16, 8192, 512, 512, True, "bf16")      # 8192 rows: both sequences
+    assert bpt.group_rows(c) == 8192 and "2 sequence(s) x 4096 rows" in bpt.describe(c)
+    c = bpt.make_config(5, 2048, 2048, 16, 8192, 1024, 1024, True, "bf16")     # 4 of 5 fit
+    assert bpt.group_rows(c) == 4 * 2048
+    c = bpt.make_config(3, 5000, 2048, 16, 8192, 1024, 1024, True, "bf16")     # only one fits: a run
+    assert bpt.group_rows(c) == 5000 and "1 sequence(s) x 5000 rows" in bpt.describe(c)
+    c = bpt.make_config(1, 100, 256, 2, 512, 10, 10, True, "bf16")             # B = 1
+    assert bpt.group_rows(c) == 100
+    c = bpt.make_config(4, 100, 256, 2, 512, 10, 10, True, "bf16")
+    c.group_blocks = 25                                                         # 250 rows: 2 sequences
+    assert bpt.group_rows(c) == 200
+
+
 def test_saved_layout_offsets():
     for dtype in ("f32", "bf16"):
         c = cfg(B=2, S=250, dtype=dtype)
