@@ -142,6 +142,19 @@ size_t bpt_workspace_bytes(const bpt_config* cfg, int backward);
 bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params* params, void* Y,
                          void* saved, void* workspace, size_t workspace_bytes, void* stream);
 
+/* bpt_layer_fwd for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc. It takes no workspace:
+ * its kernels use the library's own static device array of BPT_NOALLOC_SCRATCH_BYTES
+ * (64 MiB), one per GPU that runs it, held until the process ends. The caller still passes
+ * X, Y and `saved` (bpt_saved_bytes bytes), as for bpt_layer_fwd, with which the results
+ * are identical. A configuration whose bpt_workspace_bytes(cfg, 0) exceeds the array
+ * returns BPT_ERR_WORKSPACE before anything is launched. Allocates nothing (no hipMalloc
+ * or hipFree; its launches bypass the launch profiler). Every call on one GPU shares that
+ * GPU's array: calls that overlap on one GPU (several streams or threads) race. */
+#define BPT_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+bpt_status bpt_layer_fwd_noalloc(const bpt_config* cfg, const void* X, const bpt_params* params, void* Y,
+                                 void* saved, void* stream);
+
 /* Backward of one layer given the forward's `saved` buffer and the upstream
  * gradient dY [B, S, D]. Writes dX [B, S, D] (out_dtype) and every non-NULL
  * gradient in `grads`. As in Section 3 (the checkpointed attention scan and the

@@ -72,7 +72,8 @@ EXPORTS = ("bpt_validate", "bpt_group_rows", "bpt_saved_bytes", "bpt_saved_layou
            "bpt_layer_fwd", "bpt_layer_bwd", "bpt_status_string", "bpt_last_error", "bpt_describe",
            "bpt_profile_enable", "bpt_profile_report", "bpt_xent_validate", "bpt_xent_workspace_bytes",
            "bpt_xent_fwd", "bpt_xent_bwd", "bpt_embed_fwd", "bpt_embed_bwd", "bpt_ln_workspace_bytes",
-           "bpt_ln_fwd", "bpt_ln_bwd", "bpt_adamw_step", "bpt_bwd_qkv_grad_offset")
+           "bpt_ln_fwd", "bpt_ln_bwd", "bpt_adamw_step", "bpt_bwd_qkv_grad_offset",
+           "bpt_layer_fwd_noalloc")
 
 _lib = None
 
@@ -99,6 +100,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.bpt_workspace_bytes.restype = c_sz
     lib.bpt_layer_fwd.argtypes = [P(Config), c_vp, P(Params), c_vp, c_vp, c_vp, c_sz, c_vp]
     lib.bpt_layer_fwd.restype = c_i32
+    lib.bpt_layer_fwd_noalloc.argtypes = [P(Config), c_vp, P(Params), c_vp, c_vp, c_vp]
+    lib.bpt_layer_fwd_noalloc.restype = c_i32
     lib.bpt_layer_bwd.argtypes = [P(Config), c_vp, P(Params), c_vp, c_vp, c_vp, P(Grads), c_vp, c_sz, c_vp]
     lib.bpt_layer_bwd.restype = c_i32
     lib.bpt_bwd_qkv_grad_offset.argtypes = [P(Config), P(c_sz)]
@@ -225,6 +228,17 @@ def layer_fwd(cfg: Config, X: torch.Tensor, params: Dict[str, Optional[torch.Ten
     _check(load().bpt_layer_fwd(ctypes.byref(cfg), X.data_ptr(), ctypes.byref(p), Y.data_ptr(),
                                 saved.data_ptr(), workspace.data_ptr(), workspace.numel() * workspace.element_size(),
                                 _stream()))
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def layer_fwd_noalloc(cfg: Config, X: torch.Tensor, params: Dict[str, Optional[torch.Tensor]], Y: torch.Tensor,
+                      saved: torch.Tensor) -> None:
+    """bpt_layer_fwd_noalloc: the forward with the library's static scratch as workspace."""
+    p = params_struct(params)
+    _check(load().bpt_layer_fwd_noalloc(ctypes.byref(cfg), X.data_ptr(), ctypes.byref(p), Y.data_ptr(),
+                                        saved.data_ptr(), _stream()))
 
 
 def layer_bwd(cfg: Config, X: torch.Tensor, params: Dict[str, Optional[torch.Tensor]], saved: torch.Tensor,

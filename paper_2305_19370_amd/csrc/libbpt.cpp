@@ -251,9 +251,13 @@ hipEvent_t pool_event() {
   return g_pool[g_pool_used++];
 }
 
+// set while a call that must not allocate runs: its launches bypass the profiler, whose
+// first use creates HIP events
+thread_local bool t_noalloc = false;
+
 template <class Fn>
 hipError_t launch(const char* name, double flops, double bytes, hipStream_t s, Fn&& fn) {
-  if (!g_prof_on) return fn();
+  if (!g_prof_on || t_noalloc) return fn();
   std::lock_guard<std::mutex> lk(g_prof_mu);
   hipEvent_t a = pool_event(), b = pool_event();
   if (!a || !b || hipEventRecord(a, s) != hipSuccess) return fn();
@@ -332,6 +336,35 @@ XentWs xent_ws(const XentDims& d, void* base, int backward, int64_t* total) {
   return w;
 }
 
+}  // namespace
+
+// Workspace of bpt_layer_fwd_noalloc: the library's own device memory, one copy per GPU,
+// held until the process ends. In host code `scratch` is a stand-in for the symbol, not a
+// device address: kernels get the address hipGetSymbolAddress returns on each device.
+static constexpr size_t kScratchBytes = BPT_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+std::vector<void*> g_scratch_dev;   // scratch's address on device i (null until first use there)
+
+// scratch's address on the current device, looked up once per device
+bpt_status scratch_ptr(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(BPT_ERR_HIP, "hipGetDevice failed: %s", hipGetErrorString(e));
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if ((size_t)dev >= g_scratch_dev.size()) g_scratch_dev.resize((size_t)dev + 1, nullptr);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(BPT_ERR_HIP, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return BPT_OK;
+}
 }  // namespace
 
 extern "C" {
@@ -462,6 +495,25 @@ size_t bpt_profile_report(char* buf, size_t n) {
     buf[k] = 0;
   }
   return out.size();
+}
+
+bpt_status bpt_layer_fwd_noalloc(const bpt_config* cfg, const void* X, const bpt_params* p, void* Y, void* saved,
+                                 void* stream) {
+  bpt_status st = check(cfg);
+  if (st != BPT_OK) return st;
+  int64_t need;
+  fwd_ws(dims_of(*cfg), nullptr, &need);
+  if ((size_t)need > kScratchBytes)
+    return fail(BPT_ERR_WORKSPACE, "this configuration needs %lld workspace bytes, more than the %zu of the "
+                "static scratch of bpt_layer_fwd_noalloc (use bpt_layer_fwd with a workspace)",
+                (long long)need, kScratchBytes);
+  void* ws = nullptr;
+  if ((st = scratch_ptr(&ws)) != BPT_OK) return st;
+  struct NoAlloc {
+    NoAlloc() { t_noalloc = true; }
+    ~NoAlloc() { t_noalloc = false; }
+  } guard;
+  return bpt_layer_fwd(cfg, X, p, Y, saved, ws, kScratchBytes, stream);
 }
 
 bpt_status bpt_layer_fwd(const bpt_config* cfg, const void* X, const bpt_params* p, void* Y, void* saved,
