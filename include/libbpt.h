@@ -72,7 +72,9 @@ typedef struct {
   int32_t group_blocks;    /* query blocks per FFN group: at most group_blocks * Bq rows of */
                            /* the [., F] intermediate are live at once (a run of one         */
                            /* sequence, or several whole sequences when two or more fit);    */
-                           /* 0 = automatic (8192 rows)                                      */
+                           /* 0 = automatic: max(8192, 2^27 / F) rows rounded up to whole   */
+                           /* query blocks (a narrow FFN gets taller groups, its            */
+                           /* intermediate staying at 2^27 elements)                        */
   float ln_eps;            /* LayerNorm epsilon (biased variance), e.g. 1e-5                */
   int32_t activation;      /* bpt_activation of the FFN                                     */
   float dropout;           /* rate p in [0, 1) of dropout on the two residual branches:     */

@@ -33,7 +33,12 @@ bpt_status fail(bpt_status st, const char* fmt, ...) {
 }
 
 constexpr int64_t kAlign = 256;
-constexpr int64_t kDefaultGroupRows = 8192;   // target rows of the [., F] FFN intermediate
+// Automatic FFN group: at least 8192 rows, and for a narrow FFN as many rows as keep the
+// [., F] intermediate at 2^27 elements (256 MiB in bf16), so that the group's GEMMs are
+// tall enough to fill the chip.
+constexpr int64_t kDefaultGroupRows = 8192;
+constexpr int64_t kGroupElems = int64_t(1) << 27;
+int64_t auto_group_rows(int64_t F) { return std::max(kDefaultGroupRows, kGroupElems / std::max<int64_t>(F, 1)); }
 
 int64_t rup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 size_t esize(int32_t dt) { return dt == BPT_BF16 ? 2 : 4; }
@@ -54,7 +59,7 @@ Dims dims_of(const bpt_config& c) {
   d.Sp = rup(c.S, 64);
   d.Tp = c.B * d.Sp;
   const int64_t g = c.group_blocks > 0 ? c.group_blocks
-                                      : std::max<int64_t>(1, (kDefaultGroupRows + c.Bq - 1) / c.Bq);
+                                      : std::max<int64_t>(1, (auto_group_rows(c.F) + c.Bq - 1) / c.Bq);
   // A group holds up to g * Bq rows: a run of Rs rows of one sequence or, when at least two
   // whole sequences fit, nbg whole sequences (their tokens are contiguous), so that short
   // sequences still give the FFN GEMMs their full height.
@@ -160,19 +165,26 @@ struct BwdWs {
   float *dv, *dh, *dU, *ndelta, *nlse2, *partial, *scratch;
   void *dhe, *dhT, *dO, *dqkvT, *u;
   float* kpart;          // K-slice partials of the D x D weight gradients (null: no split)
+  float* fpart;          // K-slice partials of dW1 / dW2 (null: no split)
   void* dYm;             // dY through the FFN branch's dropout (null: no dropout)
 };
 
-// Slices of K for a D x D weight-gradient GEMM (fp32 C, plain store) over K tokens whose
-// 256 x 256 tile grid would leave most of the 256 CUs idle (D < 4096): the slices run as
-// batch entries into fp32 partials that sum_slices adds into C in a fixed order. Needs
-// K % 64 == 0 (every slice a multiple of the 32-deep K step).
-constexpr int kMaxKSplit = 4;
-int ksplit(int64_t D, int64_t K) {
-  if (K % 64 != 0) return 1;
-  const int64_t tiles = ((D + 255) / 256) * ((D + 255) / 256);
+// Slices of K for an M x N weight-gradient GEMM (fp32 C, plain store) over K tokens whose
+// 256 x 256 tile grid would leave most of the 256 CUs idle (a narrow layer: D < 4096, or
+// D x F < 256 tiles): the slices run as batch entries into fp32 partials that sum_slices
+// adds into C in a fixed order. Every slice is a multiple of 64 tokens.
+constexpr int kMaxKSplit = 16;
+int ksplit_cap(int64_t M, int64_t N) {   // the most slices the tile grid allows
+  const int64_t tiles = ((M + 255) / 256) * ((N + 255) / 256);
   int z = 1;
-  while (z < kMaxKSplit && tiles * 2 * z <= 256 && K % (64 * 2 * z) == 0) z *= 2;
+  while (z < kMaxKSplit && tiles * 2 * z <= 256) z *= 2;
+  return z;
+}
+int ksplit(int64_t M, int64_t N, int64_t K) {
+  if (K % 64 != 0) return 1;
+  const int cap = ksplit_cap(M, N);
+  int z = 1;
+  while (z < cap && K % (64 * 2 * z) == 0) z *= 2;
   return z;
 }
 
@@ -196,8 +208,10 @@ BwdWs bwd_ws(const Dims& d, void* base, int64_t* total) {
   w.dU = (float*)bp.take(d.T * d.D * 4);
   w.partial = (float*)bp.take((int64_t)layer_norm_param_grad_ws(std::max(d.D, d.F)) * 4);
   w.scratch = (float*)bp.take(2 * std::max(d.D, d.F) * 4);
-  const int kz = d.S % 64 == 0 ? ksplit(d.D, d.T) : 1;   // the whole-batch GEMMs below
+  const int kz = d.S % 64 == 0 ? ksplit(d.D, d.D, d.T) : 1;   // the whole-batch GEMMs below
   w.kpart = kz > 1 ? (float*)bp.take(kz * d.D * d.D * 4) : nullptr;
+  const int fz = ksplit_cap(d.D, d.F);                      // dW1 and dW2 per FFN group
+  w.fpart = fz > 1 ? (float*)bp.take(fz * d.D * d.F * 4) : nullptr;
   w.dYm = d.drop ? bp.take(d.T * d.D * d.E) : nullptr;
   *total = rup(bp.off, kAlign);
   return w;
@@ -683,11 +697,20 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
         RUN("gemm.bwd_dz", gemm_flops(g), gemm_bytes(g, E_, E_ + GP_), gemm(E, EPI_MUL, E, GP, g, s));
       }
       if (G.db1) RUN("reduce.bias", 0, (double)F * r * E_, row_sum(E, w.dzT, d.Rp, F, r, G.db1, first ? 0 : 1, s));
+      // K slices of the FFN weight gradients for a group of whole 64-row blocks (every slice
+      // inside the group's rows, so no clamped rows)
+      const int fz = w.fpart && r % 64 == 0 ? ksplit(D, F, r) : 1;
       if (G.dW2) {   // dW2 = G^T dY, dY read token-major (G^T is zero past the group's rows)
         GemmArgs g;
         g.A = w.gT; g.lda = d.Rp; g.B = dYg; g.ldb = D; g.trans_b = 1; g.b_rows = r;
         g.C = G.dW2; g.ldc = D; g.M = F; g.N = D; g.K = rp; g.accumulate = first ? 0 : 1;
+        if (fz > 1) {
+          g.b_rows = 0; g.batch = fz; g.K = r / fz; g.sA = g.K; g.sB = g.K * D;
+          g.C = w.fpart; g.sC = F * D; g.accumulate = 0;
+        }
         RUN("gemm.bwd_dw2", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
+        if (fz > 1)
+          RUN("reduce.ksplit", 0, (double)(fz + 1) * F * D * 4, sum_slices(w.fpart, fz, F * D, G.dW2, first ? 0 : 1, s));
       }
       {   // dv = dZ W1^T, dZ read from its feature-major copy
         GemmArgs g;
@@ -701,7 +724,13 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
         g.A = w.vg; g.lda = D; g.trans_a = 1; g.a_rows = r;
         g.B = w.dzT; g.ldb = d.Rp; g.C = G.dW1; g.ldc = F;
         g.M = D; g.N = F; g.K = rp; g.accumulate = first ? 0 : 1;
+        if (fz > 1) {
+          g.a_rows = 0; g.batch = fz; g.K = r / fz; g.sA = g.K * D; g.sB = g.K;
+          g.C = w.fpart; g.sC = D * F; g.accumulate = 0;
+        }
         RUN("gemm.bwd_dw1", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
+        if (fz > 1)
+          RUN("reduce.ksplit", 0, (double)(fz + 1) * D * F * 4, sum_slices(w.fpart, fz, D * F, G.dW1, first ? 0 : 1, s));
       }
       first = false;
     }
@@ -727,7 +756,7 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
   // token-major and the feature-major dQ^T, dK^T, dV^T unpadded over the whole batch, so
   // each D x D weight gradient is one GEMM with K = T (split along K when D < 4096).
   const bool whole = S % 64 == 0;
-  const int kz = whole && w.kpart ? ksplit(D, T) : 1;
+  const int kz = whole && w.kpart ? ksplit(D, D, T) : 1;
   auto wgrad = [&](const char* name, GemmArgs g, float* out, int64_t sa, int64_t sb) -> bpt_status {
     if (kz > 1) {   // K slices of T / kz tokens; A and B step by sa and sb elements per slice
       g.batch = kz; g.K = T / kz; g.sA = sa * g.K; g.sB = sb * g.K; g.C = w.kpart; g.sC = D * D;

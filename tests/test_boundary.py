@@ -113,9 +113,14 @@ def test_sizes_linear_in_S(dtype):
     (up to 64-token padding and 256-byte alignment)."""
     D, H, F, Bq = 1024, 8, 4096, 256
     Ss = [8192, 16384, 24576, 32768]     # multiples of 64 and of the group rows
+
+    def conf(S):
+        c = bpt.make_config(1, S, D, H, F, Bq, Bq, True, dtype)
+        c.group_blocks = 8192 // Bq         # groups of 8192 rows, fewer than S
+        return c
     for fn in (lambda c: bpt.saved_bytes(c), lambda c: bpt.workspace_bytes(c, False),
                lambda c: bpt.workspace_bytes(c, True)):
-        v = [fn(bpt.make_config(1, S, D, H, F, Bq, Bq, True, dtype)) for S in Ss]
+        v = [fn(conf(S)) for S in Ss]
         d1 = [b - a for a, b in zip(v, v[1:])]
         assert max(d1) - min(d1) <= 4096, (v, d1)
         per_token = d1[0] / 8192
@@ -127,7 +132,10 @@ def test_sizes_linear_in_S(dtype):
 
 def test_group_rows_and_describe():
     c = bpt.make_config(1, 32768, 4096, 32, 16384, 1024, 1024, True, "bf16")
-    assert bpt.group_rows(c) == 8192
+    assert bpt.group_rows(c) == 8192                    # automatic: 8192 rows at F >= 16384
+    for F, rows in ((4096, 32768), (8192, 16384), (20480, 8192)):   # else 2^27 / F rows
+        assert bpt.group_rows(bpt.make_config(1, 65536, 1024, 8, F, 1024, 1024, True, "bf16")) == rows
+    assert bpt.group_rows(bpt.make_config(1, 65536, 1024, 8, 4096, 1000, 1000, True, "bf16")) == 33000
     c.group_blocks = 1
     assert bpt.group_rows(c) == 1024
     c.group_blocks = 100
@@ -148,11 +156,13 @@ def test_group_rows_and_describe():
 def test_groups_of_whole_sequences():
     """A group holds several whole sequences when at least two fit in group_blocks * Bq
     rows (and never more sequences than the batch has); otherwise a run of one."""
-    c = bpt.make_config(2, 4096, 2048, 16, 8192, 512, 512, True, "bf16")      # 8192 rows: both sequences
+    c = bpt.make_config(2, 4096, 2048, 16, 16384, 512, 512, True, "bf16")     # 8192 rows: both sequences
     assert bpt.group_rows(c) == 8192 and "2 sequence(s) x 4096 rows" in bpt.describe(c)
-    c = bpt.make_config(5, 2048, 2048, 16, 8192, 1024, 1024, True, "bf16")     # 4 of 5 fit
+    c = bpt.make_config(5, 2048, 2048, 16, 16384, 1024, 1024, True, "bf16")    # 4 of 5 fit
     assert bpt.group_rows(c) == 4 * 2048
-    c = bpt.make_config(3, 5000, 2048, 16, 8192, 1024, 1024, True, "bf16")     # only one fits: a run
+    c = bpt.make_config(5, 2048, 2048, 16, 8192, 1024, 1024, True, "bf16")     # 16384 rows at F = 8192
+    assert bpt.group_rows(c) == 5 * 2048
+    c = bpt.make_config(3, 5000, 2048, 16, 16384, 1024, 1024, True, "bf16")    # only one fits: a run
     assert bpt.group_rows(c) == 5000 and "1 sequence(s) x 5000 rows" in bpt.describe(c)
     c = bpt.make_config(1, 100, 256, 2, 512, 10, 10, True, "bf16")             # B = 1
     assert bpt.group_rows(c) == 100
