@@ -424,6 +424,51 @@ def gemm_yardstick(args) -> int:
     return 0
 
 
+def mfma_probe(args) -> int:
+    """--mfma-probe: the matrix-core loops of libbpt_probe.so (bf16 32x32x16 products on
+    register operands, and with one LDS fragment read per product), timed over launches
+    of about 0.2 s each: the rates the chip sustains for matrix work without memory
+    traffic, beside the nominal 2.5 PFLOP/s."""
+    import ctypes
+    import torch
+    torch.cuda.set_device(0)
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2305_19370_amd", "libbpt_probe.so"))
+    fn = lib.bpt_probe_mfma_loop
+    fn.restype = ctypes.c_int32
+    fn.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                   ctypes.c_void_p]
+    seed = (torch.rand(4096, generator=torch.Generator().manual_seed(0)) * 2 - 1).cuda()
+    out = torch.empty(2048 * 256, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    # (name, mode, workgroups, iterations): 8 resident waves per SIMD for the register loops,
+    # two for the LDS-fed one (its 64 KiB of LDS per workgroup)
+    modes = (("one_pair", 0, 2048, 300000), ("varied_pairs", 1, 2048, 300000), ("lds_fragment", 2, 512, 1000000))
+    res = {}
+    for name, mode, wg, iters in modes:
+        flops = float(wg) * 4 * iters * 4 * 32768
+        ms = []
+        for i in range(args.warmup + args.steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            rc = fn(wg, iters, mode, seed.data_ptr(), out.data_ptr(), stream)
+            e1.record()
+            if rc != 0:
+                raise RuntimeError(f"bpt_probe_mfma_loop returned {rc}")
+            torch.cuda.synchronize()
+            if i >= args.warmup:
+                ms.append(e0.elapsed_time(e1))
+                print(f"[mfma-probe] {name} launch {len(ms)}: {ms[-1]:.2f} ms, {flops / ms[-1] / 1e9:.1f} TFLOP/s",
+                      file=sys.stderr, flush=True)
+        tf = [flops / m / 1e9 for m in ms]
+        res[name] = {"mode": mode, "workgroups": wg, "iters": iters, "flops_per_launch": flops,
+                     "ms": [round(m, 3) for m in ms], "tflops": [round(t, 1) for t in tf],
+                     "mean_tflops": round(sum(tf) / len(tf), 1), "min_tflops": round(min(tf), 1)}
+    assert torch.isfinite(out).all()
+    print(json.dumps({"probe": "bf16 MFMA 32x32x16 loops (libbpt_probe.so)", "peak_tflops": 2500.0, "modes": res}),
+          flush=True)
+    return 0
+
+
 def host_cpu_info(threads: int) -> dict:
     """The host CPU model and the BLAS library numpy's oracle runs on."""
     model = "unknown"
@@ -598,6 +643,8 @@ def main() -> int:
                     help="only measure the throughput of fp32 atomic adds into device memory")
     ap.add_argument("--sweep-s", default="", metavar="S1,S2,...",
                     help="measure the 13B-shaped layer at each of these sequence lengths (peak HBM vs S)")
+    ap.add_argument("--mfma-probe", action="store_true",
+                    help="time the register-only matrix-core loop (the chip's sustained bf16 MFMA rate)")
     ap.add_argument("--gemm-yardstick", action="store_true",
                     help="time torch.matmul (hipBLASLt) on the 7B-shaped layer's GEMM shapes, then run the layer")
     args = ap.parse_args()
@@ -615,6 +662,8 @@ def main() -> int:
         return bench_gpt(args)
     if args.sweep_s:
         return bench_sweep(args)
+    if args.mfma_probe:
+        return mfma_probe(args)
     if args.gemm_yardstick:
         rc = gemm_yardstick(args)
         if rc:

@@ -27,6 +27,9 @@ EXTRA_FLAGS = {
     "attn_bwd_dkdv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 LIB = os.path.join(PKG, "libbpt.so")
+# the matrix-core ceiling probe that bench.py --mfma-probe times (measurement only)
+PROBE_SOURCES = ["probe_mfma.hip"]
+PROBE_LIB = os.path.join(PKG, "libbpt_probe.so")
 ARCH = os.environ.get("BPT_OFFLOAD_ARCH", "gfx950")
 
 HIP_FLAGS = [
@@ -54,18 +57,20 @@ def _compile(src: str, obj: str) -> None:
 
 
 def build(verbose: bool = True) -> str:
+    srcs = SOURCES + PROBE_SOURCES
     with tempfile.TemporaryDirectory(prefix="bpt_build_") as tmp:
-        objs = [os.path.join(tmp, s + ".o") for s in SOURCES]
-        with concurrent.futures.ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 1)) as ex:
-            list(ex.map(_compile, SOURCES, objs))
-        out_tmp = LIB + ".tmp"
-        r = subprocess.run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", out_tmp, *objs],
-                           capture_output=True, text=True)
-        if r.returncode != 0:
-            raise RuntimeError(f"link failed:\n{r.stderr[-4000:]}")
-        os.replace(out_tmp, LIB)
-    if verbose:
-        print(f"built {LIB}", file=sys.stderr)
+        objs = {s: os.path.join(tmp, s + ".o") for s in srcs}
+        with concurrent.futures.ThreadPoolExecutor(max_workers=min(len(srcs), os.cpu_count() or 1)) as ex:
+            list(ex.map(_compile, srcs, [objs[s] for s in srcs]))
+        for lib, group in ((LIB, SOURCES), (PROBE_LIB, PROBE_SOURCES)):
+            out_tmp = lib + ".tmp"
+            r = subprocess.run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", out_tmp,
+                                *[objs[s] for s in group]], capture_output=True, text=True)
+            if r.returncode != 0:
+                raise RuntimeError(f"link of {os.path.basename(lib)} failed:\n{r.stderr[-4000:]}")
+            os.replace(out_tmp, lib)
+            if verbose:
+                print(f"built {lib}", file=sys.stderr)
     return LIB
 
 

@@ -243,3 +243,25 @@ def test_gpt_step_entries_validate_before_launch():
     for bad in (bpt.AdamWConfig(1e-3, 1.0, 0.95, 1e-8, 0.1, 1, 1), bpt.AdamWConfig(1e-3, 0.9, 0.95, 0.0, 0.1, 1, 1),
                 bpt.AdamWConfig(1e-3, 0.9, 0.95, 1e-8, 0.1, 1, 0), bpt.AdamWConfig(-1.0, 0.9, 0.95, 1e-8, 0.1, 1, 1)):
         assert lib.bpt_adamw_step(ctypes.byref(bad), 8, 4096, 8192, 12288, 16384, None, None) == 1
+
+
+def test_probe_library_exports_match_header():
+    """libbpt_probe.so (the matrix-core ceiling probe bench.py --mfma-probe times) exports
+    what include/bpt_probe.h declares, and rejects invalid arguments without launching."""
+    path = os.path.join(os.path.dirname(bpt.LIB_PATH), "libbpt_probe.so")
+    if not os.path.exists(path):
+        pytest.skip("libbpt_probe.so not built")
+    txt = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "bpt_probe.h")).read(), flags=re.S)
+    decl = sorted(set(re.findall(r"\b(bpt_[a-z_]+)\s*\(", txt)))
+    assert decl == ["bpt_probe_mfma_loop"]
+    lib = ctypes.CDLL(path)
+    fn = lib.bpt_probe_mfma_loop
+    fn.restype = ctypes.c_int32
+    fn.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                   ctypes.c_void_p]
+    assert fn(0, 10, 0, 4096, 4096, None) == 1          # no workgroups
+    assert fn(1 << 25, 10, 0, 4096, 4096, None) == 1    # too many
+    assert fn(8, 0, 0, 4096, 4096, None) == 1           # no iterations
+    assert fn(8, 10, 0, None, 4096, None) == 1          # null seed
+    assert fn(8, 10, 1, 4096, None, None) == 1          # null out
+    assert fn(8, 10, 3, 4096, 4096, None) == 1          # no such mode
