@@ -370,24 +370,30 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
     const int64_t r = k0 + row < xrows ? k0 + row : xrows - 1;
     return X + r * ld + col;
   };
-  auto dma = [&](int kt, int d) {
+  // FAST: a stage whose k rows all lie below arows and brows (no clamping of transposed rows)
+  auto dma = [&](int kt, int d, auto FASTc) {
+    constexpr bool FAST = decltype(FASTc)::value;
     const uint32_t st = ring + (kt % Cfg::NS) * Cfg::STAGE;
     const int k0 = kt * Cfg::BK;
     if (d < Cfg::APW) {
       int blk = wave + Cfg::NW * d;
       blk = blk < Cfg::ABLK ? blk : Cfg::ABLK - 1;
-      if constexpr (TA)
-        lds_dma16(tr_src(A, a.lda, arows, acols, k0, blk, aoff[d], std::integral_constant<int, BM>{}),
-                  st + blk * 1024);
-      else
+      if constexpr (TA) {
+        if constexpr (FAST) lds_dma16(A + (int64_t)k0 * a.lda + aoff[d], st + blk * 1024);
+        else
+          lds_dma16(tr_src(A, a.lda, arows, acols, k0, blk, aoff[d], std::integral_constant<int, BM>{}),
+                    st + blk * 1024);
+      } else
         lds_dma16(A + k0 + aoff[d], st + blk * 1024);
     } else {
       int blk = wave + Cfg::NW * (d - Cfg::APW);
       blk = blk < Cfg::BBLK ? blk : Cfg::BBLK - 1;
-      if constexpr (TB)
-        lds_dma16(tr_src(B, a.ldb, brows, bcols, k0, blk, boff[d - Cfg::APW], std::integral_constant<int, BN>{}),
-                  st + Cfg::ABYTES + blk * 1024);
-      else
+      if constexpr (TB) {
+        if constexpr (FAST) lds_dma16(B + (int64_t)k0 * a.ldb + boff[d - Cfg::APW], st + Cfg::ABYTES + blk * 1024);
+        else
+          lds_dma16(tr_src(B, a.ldb, brows, bcols, k0, blk, boff[d - Cfg::APW], std::integral_constant<int, BN>{}),
+                    st + Cfg::ABYTES + blk * 1024);
+      } else
         lds_dma16(B + k0 + boff[d - Cfg::APW], st + Cfg::ABYTES + blk * 1024);
     }
   };
@@ -442,7 +448,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
   // fragment read of the next k step (stage rkt, half rkk) into the other buffer and by
   // this wave's share of the copies of stage dkt, so that the LDS and copy traffic is
   // spread over the MFMA stream instead of arriving in bursts.
-  auto kstep = [&](auto cur_c, auto read_c, auto dma_c, int rkt, int rkk, int dkt) {
+  auto kstep = [&](auto cur_c, auto read_c, auto dma_c, int rkt, int rkk, int dkt, auto fast_c) {
     constexpr int cur = decltype(cur_c)::value;
     constexpr bool rd = decltype(read_c)::value, cp = decltype(dma_c)::value;
     constexpr int TMN = Cfg::TM * Cfg::TN, NR = Cfg::TM + Cfg::TN;
@@ -454,7 +460,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
       if (rd && q < NR) read_frag(rst, rkk, 1 - cur, q);
       if (cp) {
 #pragma unroll
-        for (int d = (q * Cfg::DPS + TMN - 1) / TMN; d < ((q + 1) * Cfg::DPS + TMN - 1) / TMN; ++d) dma(dkt, d);
+        for (int d = (q * Cfg::DPS + TMN - 1) / TMN; d < ((q + 1) * Cfg::DPS + TMN - 1) / TMN; ++d) dma(dkt, d, fast_c);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -469,7 +475,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
   for (int s = 0; s < Cfg::NS - 1; ++s)
     if (s < nk) {
 #pragma unroll
-      for (int d = 0; d < Cfg::DPS; ++d) dma(s, d);
+      for (int d = 0; d < Cfg::DPS; ++d) dma(s, d, F_{});
     }
   if (nk >= Cfg::NS - 1) wait_vmcnt<(Cfg::NS - 2) * Cfg::DPS>();
   else wait_vmcnt<0>();
@@ -484,22 +490,35 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
   // publishes stage kt+1, whose first half the second k step reads. The two loops differ
   // only in whether copies remain; the last stage is peeled.
   const int kcopy = nk - (Cfg::NS - 1) > 0 ? nk - (Cfg::NS - 1) : 0;
+  // stages whose copies need no clamping: all of them unless a transposed operand has
+  // fewer readable k rows than K
+  int64_t kread = a.K;
+  if constexpr (TA) kread = arows < kread ? arows : kread;
+  if constexpr (TB) kread = brows < kread ? brows : kread;
+  const int kfast = (int)(kread / Cfg::BK);     // stages 0 .. kfast-1 are whole
+  const int kc1 = kfast - (Cfg::NS - 1) < kcopy ? (kfast - (Cfg::NS - 1) > 0 ? kfast - (Cfg::NS - 1) : 0) : kcopy;
   int kt = 0;
-  for (; kt < kcopy; ++kt) {
-    kstep(I0{}, T_{}, T_{}, kt, 1, kt + Cfg::NS - 1);
+  for (; kt < kc1; ++kt) {
+    kstep(I0{}, T_{}, T_{}, kt, 1, kt + Cfg::NS - 1, T_{});
     wait_vmcnt<(Cfg::NS - 2) * Cfg::DPS>();
     __syncthreads();
-    kstep(I1{}, T_{}, F_{}, kt + 1, 0, 0);
+    kstep(I1{}, T_{}, F_{}, kt + 1, 0, 0, T_{});
+  }
+  for (; kt < kcopy; ++kt) {
+    kstep(I0{}, T_{}, T_{}, kt, 1, kt + Cfg::NS - 1, F_{});
+    wait_vmcnt<(Cfg::NS - 2) * Cfg::DPS>();
+    __syncthreads();
+    kstep(I1{}, T_{}, F_{}, kt + 1, 0, 0, F_{});
   }
   for (; kt + 1 < nk; ++kt) {
-    kstep(I0{}, T_{}, F_{}, kt, 1, 0);
+    kstep(I0{}, T_{}, F_{}, kt, 1, 0, F_{});
     wait_vmcnt<0>();
     __syncthreads();
-    kstep(I1{}, T_{}, F_{}, kt + 1, 0, 0);
+    kstep(I1{}, T_{}, F_{}, kt + 1, 0, 0, F_{});
   }
   if (nk > 0) {
-    kstep(I0{}, T_{}, F_{}, nk - 1, 1, 0);
-    kstep(I1{}, F_{}, F_{}, 0, 0, 0);
+    kstep(I0{}, T_{}, F_{}, nk - 1, 1, 0, F_{});
+    kstep(I1{}, F_{}, F_{}, 0, 0, 0, F_{});
   }
   __syncthreads();
 
