@@ -101,6 +101,35 @@ def recorded_traffic(cls: str, workload: str):
     return None
 
 
+def time_steps(step, steps: int):
+    """Time `steps` calls of step() bracketed by device synchronisations: (ms per step from
+    HIP events, wall seconds). Nothing else runs in the timed region."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps, time.perf_counter() - t0
+
+
+def profiled_steps(step, steps: int):
+    """The same `steps` steps again with libbpt's per-launch profiler on (HIP events around
+    every launch, on the stream the kernel runs on): per launch class, its launches, time
+    and algorithmic work; and the step time with the events in place (their gaps make it
+    slightly longer than the unprofiled one)."""
+    from paper_2305_19370_amd import bpt
+    bpt.profile_enable(True)
+    try:
+        ms, _ = time_steps(step, steps)
+    finally:
+        bpt.profile_enable(False)
+    return bpt.profile_report(), ms
+
+
 def copy_probe(nbytes: int, reps: int) -> int:
     """A plain device copy of nbytes (read nbytes, write nbytes), the calibration
     reference for the HBM byte counters."""
@@ -203,17 +232,9 @@ def bench_xent(args) -> int:
         step()
     torch.cuda.synchronize()
     torch.cuda.reset_peak_memory_stats()
-    bpt.profile_enable(True)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(args.steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
-    bpt.profile_enable(False)
-    prof = bpt.profile_report()
-    ms = e0.elapsed_time(e1) / args.steps
+    ms, _ = time_steps(step, args.steps)
+    peak_gib = torch.cuda.max_memory_allocated() / 2 ** 30
+    prof, ms_prof = profiled_steps(step, args.steps)
     ok = bool(torch.isfinite(loss).all() and torch.isfinite(dh.float()).all())
     print(f"[bench] xent {args.steps} steps: {ms:.2f} ms/step, loss {loss.item():.4f}, finite={ok}",
           file=sys.stderr, flush=True)
@@ -229,7 +250,8 @@ def bench_xent(args) -> int:
                    "block_rows": min(8192, T)},
         "pct_of_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "tokens_per_s": round(T / (ms / 1e3), 1),
-        "peak_hbm_gib": round(torch.cuda.max_memory_allocated() / 2 ** 30, 3),
+        "peak_hbm_gib": round(peak_gib, 3),
+        "profiled_ms_per_step": round(ms_prof, 3),
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "kernel": name,
                      "launches_per_step": rec["count"] / args.steps, "avg_launch_ms": rec["ms"] / rec["count"],
@@ -313,7 +335,7 @@ def bench_gpt(args) -> int:
     g = torch.Generator(device="cpu").manual_seed(0)
     tok = torch.randint(0, s.V, (s.B * s.S,), generator=g, dtype=torch.int32).cuda()
     tgt = torch.randint(0, s.V, (s.B * s.S,), generator=g, dtype=torch.int32).cuda()
-    total = args.warmup + args.steps
+    total = args.warmup + 2 * args.steps     # warm-up, timed and profiled steps
     it = [0]
 
     def step():
@@ -324,17 +346,9 @@ def bench_gpt(args) -> int:
         step()
     torch.cuda.synchronize()
     torch.cuda.reset_peak_memory_stats()
-    bpt.profile_enable(True)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(args.steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
-    bpt.profile_enable(False)
-    prof = bpt.profile_report()
-    ms = e0.elapsed_time(e1) / args.steps
+    ms, _ = time_steps(step, args.steps)
+    peak_gib = torch.cuda.max_memory_allocated() / 2 ** 30
+    prof, ms_prof = profiled_steps(step, args.steps)
     loss = float(m.loss.item())
     ok = bool(torch.isfinite(m.loss).all())
     print(f"[bench] gpt {args.steps} steps: {ms:.2f} ms/step, loss {loss:.4f}, finite={ok}",
@@ -364,7 +378,8 @@ def bench_gpt(args) -> int:
         "model_tflops": round(fl / (ms / 1e3) / 1e12, 2),
         "pct_of_peak": round(100 * fl / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 2),
         "loss": loss,
-        "peak_hbm_gib": round(torch.cuda.max_memory_allocated() / 2 ** 30, 3),
+        "peak_hbm_gib": round(peak_gib, 3),
+        "profiled_ms_per_step": round(ms_prof, 3),
         "roofline": roof,
         "kernels": {k: {"ms_per_step": v["ms"] / args.steps,
                         "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["flops"] > 0 and v["ms"] > 0 else None,
@@ -552,29 +567,20 @@ def measure_layer(w, steps: int, warmup: int, verbose: bool = True) -> dict:
     torch.cuda.synchronize()
     fwd_ms = e0.elapsed_time(e1) / steps
 
-    bpt.profile_enable(True)
-    torch.cuda.synchronize()
-    e0.record()
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    bpt.profile_enable(False)
-    prof = bpt.profile_report()
-    ms = e0.elapsed_time(e1) / steps
+    ms, wall = time_steps(step, steps)
     peak = torch.cuda.max_memory_allocated() - base
+    prof, ms_prof = profiled_steps(step, steps)
     ok = bool(torch.isfinite(Y.float()).all() and torch.isfinite(dX.float()).all())
     bufs = layer_buffers(w, cfg, bpt)
     group_rows = bpt.group_rows(cfg)
     del d, wsf, wsb, Y, dX, saved, grads
     torch.cuda.empty_cache()
     if verbose:
-        print(f"[bench] {w.name} {steps} steps: {ms:.2f} ms/step (wall {wall / steps * 1e3:.2f}), fwd {fwd_ms:.2f} ms, "
+        print(f"[bench] {w.name} {steps} steps: {ms:.2f} ms/step (wall {wall / steps * 1e3:.2f}; "
+              f"{ms_prof:.2f} with per-launch events), fwd {fwd_ms:.2f} ms, "
               f"peak {peak / 2 ** 30:.3f} GiB, finite={ok}", file=sys.stderr, flush=True)
     return {"ms": ms, "fwd_ms": fwd_ms, "peak": peak, "buffers": bufs, "prof": prof, "ok": ok,
-            "group_rows": group_rows}
+            "group_rows": group_rows, "ms_profiled": ms_prof}
 
 
 def linear_fit(xs, ys):
@@ -720,6 +726,7 @@ def main() -> int:
         "fwd_tflops": round(ffwd / (fwd_ms / 1e3) / 1e12, 2),
         "peak_hbm_gib": round(peak_hbm / 2 ** 30, 3),
         "expected_hbm_gib": round(sum(r["buffers"].values()) / 2 ** 30, 3),
+        "profiled_ms_per_step": round(r["ms_profiled"], 3),
         "roofline": roof,
         "kernels": breakdown,
     }
