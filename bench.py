@@ -62,12 +62,12 @@ def cpu_baseline(w, sample_S: int):
             "seconds": dt, "host": host_cpu_info(threads)}
 
 
-# Sources whose every byte defines a launch class's kernel: a recorded HBM-traffic
-# measurement of that class applies only while their hash is unchanged.
+# Sources whose every byte defines a launch class's kernel, and the compile flags of its
+# translation unit: a recorded HBM-traffic measurement of that class applies only while
+# their hash is unchanged.
 TRAFFIC_SOURCES = {
     cls: ["paper_2305_19370_amd/csrc/" + f, "paper_2305_19370_amd/csrc/attn_common.h",
-          "paper_2305_19370_amd/csrc/common.h", "paper_2305_19370_amd/csrc/internal.h",
-          "paper_2305_19370_amd/build.py"]
+          "paper_2305_19370_amd/csrc/common.h", "paper_2305_19370_amd/csrc/internal.h"]
     for cls, f in (("attn.bwd_dkdv", "attn_bwd_dkdv.hip"), ("attn.bwd_dq", "attn_bwd_dq.hip"),
                    ("attn.fwd", "attn_fwd.hip"))
 }
@@ -76,12 +76,17 @@ TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "attn_kernels_7b_s32768_hbm_traf
 
 def source_hash(cls: str):
     import hashlib
+    from paper_2305_19370_amd import build
     if cls not in TRAFFIC_SOURCES:
         return None
     h = hashlib.sha256()
     for f in TRAFFIC_SOURCES[cls]:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
+    unit = os.path.basename(TRAFFIC_SOURCES[cls][0])
+    flags = build.HIP_FLAGS + build.EXTRA_FLAGS.get(unit, [])
+    flags = [f for i, f in enumerate(flags) if f != "-I" and (i == 0 or flags[i - 1] != "-I")]  # no paths
+    h.update(" ".join(flags).encode())
     return h.hexdigest()[:16]
 
 
