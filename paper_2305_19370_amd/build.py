@@ -18,9 +18,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 SOURCES = ["libbpt.cpp", "gemm.hip", "attn_fwd.hip", "attn_bwd_dq.hip", "attn_bwd_dkdv.hip", "rowwise.hip", "gpt.hip", "dropout.hip"]
 # per-source code generation options: the attention kernels keep the accumulators of
-# their builtin MFMAs in architectural VGPRs (the default placement copies them
-# between register files every iteration; their long-lived accumulators are AGPRs
-# managed by inline assembly)
+# their MFMAs in architectural VGPRs (the default placement copies them between the
+# register files every iteration)
 EXTRA_FLAGS = {
     "attn_fwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "attn_bwd_dq.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],

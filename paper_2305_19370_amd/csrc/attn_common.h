@@ -178,33 +178,6 @@ BPT_DEV bf16x8 acc_to_b(const f32x16& s, int hf) {
   return r;
 }
 
-// 32x32x16 bf16 MFMA whose accumulator lives in AGPRs for its whole lifetime (the
-// compiler's own placement would copy it through VGPRs every iteration when VGPRs
-// are scarce). Five wait states before the MFMA cover a VALU write of its operands.
-BPT_DEV void mfma_agpr(f32x16& acc, const bf16x8& a, const bf16x8& b) {
-  asm("s_nop 4\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
-// Zero an AGPR accumulator (an MFMA of zero operands with a zero addend), so that
-// every definition of the accumulator is an AGPR one. The compiler cannot see the
-// MFMA inside the asm, so the asm itself provides the wait states after the VALU
-// write of the zero operand.
-BPT_DEV void mfma_agpr_zero(f32x16& acc) {
-  const bf16x8 z = {};
-  asm volatile("s_nop 4\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %1, 0" : "=a"(acc) : "v"(z));
-}
-// Wait states between the last mfma_agpr on these accumulators and any other use.
-BPT_DEV void mfma_agpr_drain(f32x16& a0, f32x16& a1, f32x16& a2, f32x16& a3) {
-  asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 7" : "+a"(a0), "+a"(a1), "+a"(a2), "+a"(a3));
-}
-BPT_DEV void mfma_agpr_drain(f32x16& a0, f32x16& a1) {
-  asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 7" : "+a"(a0), "+a"(a1));
-}
-template <int DT>
-BPT_DEV void drain_all(f32x16 (&a)[DT]) {
-  if constexpr (DT == 4) mfma_agpr_drain(a[0], a[1], a[2], a[3]);
-  else mfma_agpr_drain(a[0], a[1]);
-}
-
 // Row of accumulator register r for lane `lane` inside a 32x32 tile.
 BPT_DEV int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
