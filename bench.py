@@ -664,8 +664,8 @@ def main() -> int:
     if args.atomic_probe:
         return atomic_probe(args.steps)
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
-              "sharding of the layer is a design, not part of this build", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the library runs the "
+              "layer on one GPU; sharding it over several is designed, not implemented", file=sys.stderr)
         return 2
     if args.xent:
         return bench_xent(args)
