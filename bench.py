@@ -623,7 +623,10 @@ def bench_sweep(args) -> int:
                     "avoided_scores_bytes": 2 * w.B * w.H * S * S,          # one [B, H, S, S] bf16
                     "avoided_ffn_bytes": 2 * w.B * S * w.F, "finite": r["ok"]})
         del r
-    a, b, r2 = linear_fit([p["S"] for p in pts], [p["peak_hbm_bytes"] for p in pts])
+    if len({p["S"] for p in pts}) >= 2:
+        a, b, r2 = linear_fit([p["S"] for p in pts], [p["peak_hbm_bytes"] for p in pts])
+    else:                                             # one length: no fit
+        a = b = r2 = None
     out = {"metric": "BPT layer fwd+bwd TFLOP/s, tokens/s and peak HBM against sequence length (13B-shaped)",
            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
            "config": {"workload": "bf16_13b_sweep", "B": 1, "D": 5120, "H": 40, "F": 20480, "Bq": 2048,
