@@ -623,8 +623,12 @@ def bench_sweep(args) -> int:
                     "avoided_scores_bytes": 2 * w.B * w.H * S * S,          # one [B, H, S, S] bf16
                     "avoided_ffn_bytes": 2 * w.B * S * w.F, "finite": r["ok"]})
         del r
-    if len({p["S"] for p in pts}) >= 2:
-        a, b, r2 = linear_fit([p["S"] for p in pts], [p["peak_hbm_bytes"] for p in pts])
+    # the fit covers the lengths at which the FFN group has its full size (at shorter ones the
+    # group is the whole sequence, so its constant part is smaller)
+    full = max(p["group_rows"] for p in pts)
+    fit_pts = [p for p in pts if p["group_rows"] == full]
+    if len({p["S"] for p in fit_pts}) >= 2:
+        a, b, r2 = linear_fit([p["S"] for p in fit_pts], [p["peak_hbm_bytes"] for p in fit_pts])
     else:                                             # one length: no fit
         a = b = r2 = None
     out = {"metric": "BPT layer fwd+bwd TFLOP/s, tokens/s and peak HBM against sequence length (13B-shaped)",
@@ -632,7 +636,8 @@ def bench_sweep(args) -> int:
            "config": {"workload": "bf16_13b_sweep", "B": 1, "D": 5120, "H": 40, "F": 20480, "Bq": 2048,
                       "Bkv": 2048, "causal": True},
            "points": pts,
-           "peak_hbm_fit": {"intercept_bytes": a, "bytes_per_token": b, "r2": r2}}
+           "peak_hbm_fit": {"intercept_bytes": a, "bytes_per_token": b, "r2": r2,
+                            "lengths": [p["S"] for p in fit_pts]}}
     print(json.dumps(out), flush=True)
     return 0 if all(p["finite"] for p in pts) else 1
 

@@ -72,7 +72,7 @@ typedef struct {
   int32_t group_blocks;    /* query blocks per FFN group: at most group_blocks * Bq rows of */
                            /* the [., F] intermediate are live at once (a run of one         */
                            /* sequence, or several whole sequences when two or more fit);    */
-                           /* 0 = automatic: max(8192, 2^27 / F) rows rounded up to whole   */
+                           /* 0 = automatic: max(16384, 2^27 / F) rows rounded up to whole  */
                            /* query blocks (a narrow FFN gets taller groups, its            */
                            /* intermediate staying at 2^27 elements)                        */
   float ln_eps;            /* LayerNorm epsilon (biased variance), e.g. 1e-5                */

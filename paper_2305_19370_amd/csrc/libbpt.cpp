@@ -33,10 +33,10 @@ bpt_status fail(bpt_status st, const char* fmt, ...) {
 }
 
 constexpr int64_t kAlign = 256;
-// Automatic FFN group: at least 8192 rows, and for a narrow FFN as many rows as keep the
+// Automatic FFN group: at least 16384 rows, and for a narrow FFN as many rows as keep the
 // [., F] intermediate at 2^27 elements (256 MiB in bf16), so that the group's GEMMs are
-// tall enough to fill the chip.
-constexpr int64_t kDefaultGroupRows = 8192;
+// tall enough to fill the chip and few enough that their per-launch costs stay small.
+constexpr int64_t kDefaultGroupRows = 16384;
 constexpr int64_t kGroupElems = int64_t(1) << 27;
 int64_t auto_group_rows(int64_t F) { return std::max(kDefaultGroupRows, kGroupElems / std::max<int64_t>(F, 1)); }
 

@@ -17,8 +17,8 @@ dY, full size) can be compared on:
     positions (errors normalised by the RMS of the reference at the sampled positions);
 
 The selected rows (about 270) are spread over the query tiles of three windows of
-8192 rows (one automatic FFN group at the 7B and 13B shapes, a quarter of one at the RL
-shape): the start, the middle and the end of the sequence, plus the first and last two
+8192 rows (half an automatic FFN group at the 7B and 13B shapes, a quarter of one at the
+RL shape): the start, the middle and the end of the sequence, plus the first and last two
 tokens, so that the attention backward sees nonzero gradients on query tiles of every
 part of the causal triangle.
 
@@ -47,7 +47,7 @@ SEED = 0
 GRADS = ("dWq", "dWk", "dWv", "dWo", "dW1", "dW2", "db1", "db2", "dln1_g", "dln1_b", "dln2_g", "dln2_b")
 
 
-GROUP_ROWS = 8192          # window rows: one automatic FFN group at F >= 16384
+GROUP_ROWS = 8192          # window rows (half an automatic FFN group at F >= 8192)
 PER_WINDOW = 88
 
 

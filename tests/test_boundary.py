@@ -132,8 +132,8 @@ def test_sizes_linear_in_S(dtype):
 
 def test_group_rows_and_describe():
     c = bpt.make_config(1, 32768, 4096, 32, 16384, 1024, 1024, True, "bf16")
-    assert bpt.group_rows(c) == 8192                    # automatic: 8192 rows at F >= 16384
-    for F, rows in ((4096, 32768), (8192, 16384), (20480, 8192)):   # else 2^27 / F rows
+    assert bpt.group_rows(c) == 16384                   # automatic: 16384 rows at F >= 8192
+    for F, rows in ((2048, 65536), (4096, 32768), (8192, 16384), (20480, 16384)):   # else 2^27 / F
         assert bpt.group_rows(bpt.make_config(1, 65536, 1024, 8, F, 1024, 1024, True, "bf16")) == rows
     assert bpt.group_rows(bpt.make_config(1, 65536, 1024, 8, 4096, 1000, 1000, True, "bf16")) == 33000
     c.group_blocks = 1
@@ -158,12 +158,15 @@ def test_groups_of_whole_sequences():
     rows (and never more sequences than the batch has); otherwise a run of one."""
     c = bpt.make_config(2, 4096, 2048, 16, 16384, 512, 512, True, "bf16")     # 8192 rows: both sequences
     assert bpt.group_rows(c) == 8192 and "2 sequence(s) x 4096 rows" in bpt.describe(c)
-    c = bpt.make_config(5, 2048, 2048, 16, 16384, 1024, 1024, True, "bf16")    # 4 of 5 fit
+    c = bpt.make_config(5, 2048, 2048, 16, 16384, 1024, 1024, True, "bf16")    # 16384 rows: all 5
+    assert bpt.group_rows(c) == 5 * 2048
+    c = bpt.make_config(5, 2048, 2048, 16, 16384, 1024, 1024, True, "bf16")
+    c.group_blocks = 8                                                          # 8192 rows: 4 of 5 fit
     assert bpt.group_rows(c) == 4 * 2048
     c = bpt.make_config(5, 2048, 2048, 16, 8192, 1024, 1024, True, "bf16")     # 16384 rows at F = 8192
     assert bpt.group_rows(c) == 5 * 2048
-    c = bpt.make_config(3, 5000, 2048, 16, 16384, 1024, 1024, True, "bf16")    # only one fits: a run
-    assert bpt.group_rows(c) == 5000 and "1 sequence(s) x 5000 rows" in bpt.describe(c)
+    c = bpt.make_config(3, 9000, 2048, 16, 16384, 1000, 1000, True, "bf16")    # only one fits: a run
+    assert bpt.group_rows(c) == 9000 and "1 sequence(s) x 9000 rows" in bpt.describe(c)
     c = bpt.make_config(1, 100, 256, 2, 512, 10, 10, True, "bf16")             # B = 1
     assert bpt.group_rows(c) == 100
     c = bpt.make_config(4, 100, 256, 2, 512, 10, 10, True, "bf16")
