@@ -401,7 +401,8 @@ def bench_gpt(args) -> int:
 
 
 # GEMM shapes (name, M, N, K, A transposed) of the 7B-shaped layer (T = 32768 tokens, D = 4096,
-# F = 16384, FFN groups of 8192 rows), as C[M, N] = A[M, K] B[K, N]
+# F = 16384) with FFN groups of 8192 rows (the shapes the hipBLASLt comparison was taken on), as
+# C[M, N] = A[M, K] B[K, N]
 YARDSTICK_SHAPES = (
     ("qkv_proj", 32768, 4096, 4096, False),
     ("ffn1", 8192, 16384, 4096, False),
