@@ -602,6 +602,19 @@ def linear_fit(xs, ys):
     return a, b, 1.0 - ss_res / ss_tot if ss_tot > 0 else 1.0
 
 
+def peak_hbm_fit(pts) -> dict:
+    """Least-squares fit of peak HBM in S over the sweep lengths at which the FFN group has
+    its full size (at shorter ones the group is the whole sequence, so the constant part of
+    the memory is smaller); no fit with fewer than two such lengths."""
+    full = max(p["group_rows"] for p in pts)
+    fit_pts = [p for p in pts if p["group_rows"] == full]
+    lengths = [p["S"] for p in fit_pts]
+    if len(set(lengths)) < 2:
+        return {"intercept_bytes": None, "bytes_per_token": None, "r2": None, "lengths": lengths}
+    a, b, r2 = linear_fit(lengths, [p["peak_hbm_bytes"] for p in fit_pts])
+    return {"intercept_bytes": a, "bytes_per_token": b, "r2": r2, "lengths": lengths}
+
+
 def bench_sweep(args) -> int:
     """--sweep-s: the 13B-shaped layer at each sequence length of the list: fwd and
     fwd+bwd TFLOP/s, tokens/s, peak HBM against the analytic sum of the step's buffers,
@@ -624,21 +637,13 @@ def bench_sweep(args) -> int:
                     "avoided_scores_bytes": 2 * w.B * w.H * S * S,          # one [B, H, S, S] bf16
                     "avoided_ffn_bytes": 2 * w.B * S * w.F, "finite": r["ok"]})
         del r
-    # the fit covers the lengths at which the FFN group has its full size (at shorter ones the
-    # group is the whole sequence, so its constant part is smaller)
-    full = max(p["group_rows"] for p in pts)
-    fit_pts = [p for p in pts if p["group_rows"] == full]
-    if len({p["S"] for p in fit_pts}) >= 2:
-        a, b, r2 = linear_fit([p["S"] for p in fit_pts], [p["peak_hbm_bytes"] for p in fit_pts])
-    else:                                             # one length: no fit
-        a = b = r2 = None
+    fit = peak_hbm_fit(pts)
     out = {"metric": "BPT layer fwd+bwd TFLOP/s, tokens/s and peak HBM against sequence length (13B-shaped)",
            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
            "config": {"workload": "bf16_13b_sweep", "B": 1, "D": 5120, "H": 40, "F": 20480, "Bq": 2048,
                       "Bkv": 2048, "causal": True},
            "points": pts,
-           "peak_hbm_fit": {"intercept_bytes": a, "bytes_per_token": b, "r2": r2,
-                            "lengths": [p["S"] for p in fit_pts]}}
+           "peak_hbm_fit": fit}
     print(json.dumps(out), flush=True)
     return 0 if all(p["finite"] for p in pts) else 1
 

@@ -42,3 +42,13 @@ def test_recorded_traffic_applies_only_to_matching_hash(tmp_path, monkeypatch):
     assert bench.recorded_traffic("gemm.qkv", "bf16_7b_s32768") is None       # no record kept
     monkeypatch.setattr(bench, "TRAFFIC_RECORD", os.path.join(str(tmp_path), "missing.md"))
     assert bench.recorded_traffic("attn.fwd", "bf16_7b_s32768") is None
+
+
+def test_peak_hbm_fit_uses_lengths_with_full_groups():
+    pts = [{"S": S, "group_rows": min(S, 16384), "peak_hbm_bytes": (1e9 if S < 16384 else 5e9) + 2.5e5 * S}
+           for S in (8192, 16384, 32768, 65536)]
+    fit = bench.peak_hbm_fit(pts)
+    assert fit["lengths"] == [16384, 32768, 65536]
+    assert abs(fit["bytes_per_token"] - 2.5e5) < 1e-3 and abs(fit["intercept_bytes"] - 5e9) < 1.0
+    one = bench.peak_hbm_fit([{"S": 524288, "group_rows": 16384, "peak_hbm_bytes": 1.3e11}])
+    assert one["bytes_per_token"] is None and one["lengths"] == [524288]
