@@ -68,6 +68,7 @@ CASES = [
     ("s160_b2", dict(B=2, S=160, D=256, H=2, F=512, causal=True), dict(seed=12), {}),
     ("repeat_s700", dict(B=2, S=700, D=256, H=4, F=512, causal=True), dict(seed=10, affine=True, biases=True), {}),
     ("smoke_s200", dict(B=1, S=200, D=256, H=2, F=512, causal=True), dict(seed=0), {}),
+    ("ksplit_s512_b2", dict(B=2, S=512, D=256, H=2, F=1024, causal=True), dict(seed=14, affine=True, biases=True), {}),
 ]
 FULL_CASES = [("workload_1b_s4096", "bf16_1b_s4096", dict(seed=0), {})]
 # the input sets of the fp32 GPU parity tests
@@ -85,6 +86,8 @@ FP32_CASES = [
     ("f32_short_s63", dict(B=2, S=63, D=256, H=2, F=512, causal=True), dict(seed=83, affine=True, biases=True), {}),
     ("f32_s96_b2", dict(B=2, S=96, D=256, H=2, F=512, causal=True), dict(seed=12), {}),
     ("f32_s160_b2", dict(B=2, S=160, D=256, H=2, F=512, causal=True), dict(seed=12), {}),
+    ("f32_ksplit_s512_b2", dict(B=2, S=512, D=256, H=2, F=1024, causal=True), dict(seed=14, affine=True, biases=True),
+     {}),
 ]
 FP32_FULL_CASES = [("f32_workload_s512", "fp32_s512_d256", dict(seed=0), {})]
 FP32_VARIANTS = {

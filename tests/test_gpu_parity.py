@@ -255,6 +255,22 @@ def test_sequence_of_32_mod_64(dtype, S):
     compare_all(w, inp, gpu, Yr, g, "fp32" if dtype == "f32" else "bf16", w.name)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("groups", [0, 2])
+def test_weight_gradients_split_along_tokens(dtype, groups):
+    """D = 256, F = 1024, S = 512: the weight-gradient tile grids are small, so the
+    contractions over tokens run in slices summed in a fixed order. The D x D gradients
+    take 16 slices of 64 tokens over the whole batch; dW1 and dW2 take 16 slices of the
+    group's rows with automatic grouping (one group) and 4 slices per group of two
+    128-row query blocks, each group's sum added to the previous groups'."""
+    w = small_workload(dtype, B=2, S=512, D=256, H=2, F=1024, causal=True, Bq=128, Bkv=128)
+    inp = make_inputs(w, seed=14, affine=True, biases=True)
+    say(f"case token-split weight gradients {w.name} groups={groups}")
+    gpu = run_gpu(w, inp, group_blocks=groups)
+    Yr, _, g = run_oracle(w, inp)
+    compare_all(w, inp, gpu, Yr, g, "fp32" if dtype == "f32" else "bf16", f"{w.name} groups={groups}")
+
+
 def test_bf16_workload_1b_s4096():
     """The full 1B-shaped workload (B=2, S=4096, D=2048, H=16, F=8192), every output
     and gradient, and dQ, dK, dV, against the unblocked fp64 oracle."""
