@@ -447,9 +447,9 @@ def gemm_yardstick(args) -> int:
 
 def mfma_probe(args) -> int:
     """--mfma-probe: the matrix-core loops of libbpt_probe.so (bf16 32x32x16 products on
-    register operands, and with one LDS fragment read per product), timed over launches
-    of about 0.2 s each: the rates the chip sustains for matrix work without memory
-    traffic, beside the nominal 2.5 PFLOP/s."""
+    register operands, and with one LDS fragment read per one or two products, at one or
+    two waves per SIMD), timed over launches of about 0.2 s each: the rates the chip
+    sustains for matrix work without memory traffic, beside the nominal 2.5 PFLOP/s."""
     import ctypes
     import torch
     torch.cuda.set_device(0)
@@ -461,9 +461,13 @@ def mfma_probe(args) -> int:
     seed = (torch.rand(4096, generator=torch.Generator().manual_seed(0)) * 2 - 1).cuda()
     out = torch.empty(2048 * 256, device="cuda")
     stream = torch.cuda.current_stream().cuda_stream
-    # (name, mode, workgroups, iterations): 8 resident waves per SIMD for the register loops,
-    # two for the LDS-fed one (its 64 KiB of LDS per workgroup)
-    modes = (("one_pair", 0, 2048, 300000), ("varied_pairs", 1, 2048, 300000), ("lds_fragment", 2, 512, 1000000))
+    # (name, mode, workgroups, iterations): 8 resident waves per SIMD for the register loops
+    # 0 and 1, two for the LDS-fed ones 2-4 (64 KiB of LDS per workgroup), one for 5-7
+    # (96 KiB); about 0.2 s per launch
+    modes = (("one_pair", 0, 2048, 300000), ("varied_pairs", 1, 2048, 300000), ("lds_fragment", 2, 512, 1000000),
+             ("lds_fragment_ahead", 3, 512, 1000000), ("lds_half_ahead", 4, 512, 1000000),
+             ("lds_fragment_ahead_1w", 5, 256, 2000000), ("lds_half_ahead_1w", 6, 256, 2000000),
+             ("varied_pairs_1w", 7, 256, 2000000))
     res = {}
     for name, mode, wg, iters in modes:
         flops = float(wg) * 4 * iters * 4 * 32768

@@ -267,4 +267,5 @@ def test_probe_library_exports_match_header():
     assert fn(8, 0, 0, 4096, 4096, None) == 1           # no iterations
     assert fn(8, 10, 0, None, 4096, None) == 1          # null seed
     assert fn(8, 10, 1, 4096, None, None) == 1          # null out
-    assert fn(8, 10, 3, 4096, 4096, None) == 1          # no such mode
+    assert fn(8, 10, 8, 4096, 4096, None) == 1          # no such mode
+    assert fn(8, 10, -1, 4096, 4096, None) == 1         # no such mode
