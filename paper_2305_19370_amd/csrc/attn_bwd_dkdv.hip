@@ -36,7 +36,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int S = (int)a.S;
   int hh, blk;
-  xcd_map((int)blockIdx.x, a.H * a.B, hh, blk);
+  xcd_map_heads((int)blockIdx.x, a.H * a.B, (S + C::KEYS - 1) / C::KEYS, hh, blk);
   const int h = hh % a.H, b = hh / a.H;
   const int k0 = blk * C::KEYS;                     // causal: low key blocks have the most queries
   const int kw = k0 + 32 * wave;                    // first key of this wave

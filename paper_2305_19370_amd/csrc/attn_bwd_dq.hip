@@ -33,7 +33,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
   const int S = (int)a.S;
   const int nblk = (S + C::QROWS - 1) / C::QROWS;
   int hh, blk;
-  xcd_map((int)blockIdx.x, a.H * a.B, hh, blk);
+  xcd_map_heads((int)blockIdx.x, a.H * a.B, nblk, hh, blk);
   const int h = hh % a.H, b = hh / a.H;
   const int qt = a.causal ? nblk - 1 - blk : blk;   // causal: the blocks with the most keys first
   const int q0 = qt * C::QROWS;

@@ -196,6 +196,32 @@ BPT_DEV void xcd_map(int id, int NH, int& hh, int& blk) {
   }
 }
 
+// xcd_map for kernels whose heads have many blocks (nblk >= 128): when NH is a multiple
+// of 8, XCD x serves its heads x, x + 8, ... in turns of 32 consecutive blocks (blocks
+// 0 .. 31 of each of its heads, then blocks 32 .. 63 of each, ...; the last turn may be
+// shorter). The 32 workgroups an XCD holds at once then mostly belong to one head and
+// walk the same tiles together, so that fewer of the tiles they stream are fetched
+// from HBM again, while the turns still start the blocks with the most work first.
+// With fewer blocks per head the turns would mix heavy and light blocks within one
+// generation of workgroups, and xcd_map's order is kept.
+BPT_DEV void xcd_map_heads(int id, int NH, int nblk, int& hh, int& blk) {
+  constexpr int CHUNK = 32;
+  if ((NH & 7) != 0 || nblk < 4 * CHUNK) {
+    xcd_map(id, NH, hh, blk);
+    return;
+  }
+  const int x = id & 7, k = id >> 3, hp = NH >> 3;
+  const int full = nblk / CHUNK;                // turns of a whole chunk per head
+  int turn = k / (hp * CHUNK), c = CHUNK;
+  if (turn >= full) {                           // the last, shorter turn
+    turn = full;
+    c = nblk - full * CHUNK;
+  }
+  const int r = k - turn * hp * CHUNK;
+  hh = x + 8 * (r / c);
+  blk = turn * CHUNK + r % c;
+}
+
 template <typename K>
 static hipError_t set_lds(K kern, int bytes) {
   return hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
