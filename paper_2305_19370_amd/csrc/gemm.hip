@@ -322,8 +322,9 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
   const int bcols = (int)((a.b_cols > 0 ? a.b_cols : a.N) - n0);
 
   // per-lane source offsets (elements) of this wave's copy slots; rows past the
-  // matrix edge are clamped to its last row (their results are never stored)
-  int aoff[Cfg::APW], boff[Cfg::BPW];
+  // matrix edge are clamped to its last row (their results are never stored). 64-bit:
+  // a row-major operand's stride can be the token count, and 255 rows of it exceed 2^31.
+  int64_t aoff[Cfg::APW], boff[Cfg::BPW];
   {
     const int alast = (int)(a.M - 1 - m0), blast = (int)(a.N - 1 - n0);
 #pragma unroll
@@ -334,10 +335,10 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
       if constexpr (TA) {
         int row, col;
         tr_slot<BM>(slot, row, col, acols);
-        aoff[i] = row * (int)a.lda + col;
+        aoff[i] = row * a.lda + col;
       } else {
         const int row = slot >> 2, col = (slot & 3) ^ swz(row);
-        aoff[i] = (row < alast ? row : alast) * (int)a.lda + col * 8;
+        aoff[i] = (row < alast ? row : alast) * a.lda + col * 8;
       }
     }
 #pragma unroll
@@ -348,10 +349,10 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
       if constexpr (TB) {
         int row, col;
         tr_slot<BN>(slot, row, col, bcols);
-        boff[i] = row * (int)a.ldb + col;
+        boff[i] = row * a.ldb + col;
       } else {
         const int row = slot >> 2, col = (slot & 3) ^ swz(row);
-        boff[i] = (row < blast ? row : blast) * (int)a.ldb + col * 8;
+        boff[i] = (row < blast ? row : blast) * a.ldb + col * 8;
       }
     }
   }
@@ -361,7 +362,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void gemm_bf16_kernel(GemmArgs a) {
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem);
   // A transposed operand's stage is k rows k0 .. k0+31; rows from x_rows on are clamped to
   // the last readable row (the caller guarantees the other operand is zero there).
-  auto tr_src = [&](const bf16* X, int64_t ld, int64_t xrows, int cols, int k0, int blk, int off,
+  auto tr_src = [&](const bf16* X, int64_t ld, int64_t xrows, int cols, int k0, int blk, int64_t off,
                     auto BXc) -> const bf16* {
     constexpr int BX = decltype(BXc)::value;
     if (k0 + Cfg::BK <= xrows) return X + (int64_t)k0 * ld + off;
