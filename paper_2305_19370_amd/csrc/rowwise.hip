@@ -470,7 +470,7 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* in, int64_t ld_
                                                         int64_t cols, int64_t rows_store) {
   __shared__ T tile[64][65];
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;   // rows on x: no 65535 limit
   in += (int64_t)blockIdx.z * s_in;
   out += (int64_t)blockIdx.z * s_out;
 #pragma unroll
@@ -697,7 +697,7 @@ hipError_t transpose(Dt t, const void* in, int64_t ld_in, int64_t s_in, void* ou
                      int64_t s_out, int64_t rows, int64_t cols, int64_t rows_store, int batch,
                      hipStream_t s) {
   if (cols <= 0 || rows_store <= 0 || batch <= 0) return hipSuccess;
-  const dim3 grid((unsigned)((cols + 63) / 64), (unsigned)((rows_store + 63) / 64), (unsigned)batch);
+  const dim3 grid((unsigned)((rows_store + 63) / 64), (unsigned)((cols + 63) / 64), (unsigned)batch);
   BPT_T(t, T, hipLaunchKernelGGL((transpose_kernel<T>), grid, dim3(256), 0, s, (const T*)in, ld_in, s_in,
                                  (T*)out, ld_out, s_out, rows, cols, rows_store));
   return hipGetLastError();
