@@ -832,10 +832,12 @@ bpt_status bpt_layer_bwd(const bpt_config* cfg, const void* X, const bpt_params*
       }
     }
   }
-  for (int b = 0; b < B; ++b) {
-    GemmArgs g;   // dU = [dQ dK dV] [Wq Wk Wv]^T per sequence, [dQ dK dV] read feature-major
+  // dU = [dQ dK dV] [Wq Wk Wv]^T, [dQ dK dV] read feature-major: one GEMM over the batch
+  // when its columns are contiguous (S % 64 == 0), else one per sequence
+  for (int b = 0; b < (whole ? 1 : B); ++b) {
+    GemmArgs g;
     g.A = off(w.dqkvT, b * Sp * E_); g.lda = Tp; g.trans_a = 1; g.a_cols = Tp - b * Sp;
-    g.B = w.wcat; g.ldb = 3 * D; g.C = w.dU + b * S * D; g.ldc = D; g.M = S; g.N = D; g.K = 3 * D;
+    g.B = w.wcat; g.ldb = 3 * D; g.C = w.dU + b * S * D; g.ldc = D; g.M = whole ? T : S; g.N = D; g.K = 3 * D;
     RUN("gemm.bwd_du", gemm_flops(g), gemm_bytes(g, E_, 4), gemm(E, EPI_STORE, F32, F32, g, s));
   }
   RUN("layernorm.bwd", 0, (double)T * D * (E_ + 4 + 4 + EO),
