@@ -70,6 +70,8 @@ WORKLOADS: Dict[str, Workload] = {
                  "GPT 13B-shaped layer, long context (S swept 8K..64K)"),
         Workload("bf16_rl_s96000", 4, 96000, 1024, 8, 4096, True, 1024, 1024, "bf16", "unit",
                  "RL trajectories: 32 x 1000 x (return, state, action)"),
+        Workload("bf16_dh64_nc_s32768", 1, 32768, 2048, 32, 8192, False, 1024, 1024, "bf16", "unit",
+                 "1B-width layer with heads of 64, without the causal mask, long context (parity case)"),
     ]
 }
 

@@ -1,7 +1,8 @@
 """Writes the expected values of the full-size sampled parity tests — run on the CPU.
 
 For each long-context workload (the 7B-, RL- and 13B-shaped layers at their full
-sequence lengths, and the 13B-shaped layer at two shorter lengths of its sweep) the
+sequence lengths, the 13B-shaped layer at two shorter lengths of its sweep, and a
+1B-width layer with heads of 64 and no causal mask at S = 32768) the
 float64 rows oracle (``oracle/rows.py``: the plain layer definition restricted to
 selected query rows) is evaluated on the seeded inputs of
 ``bpt_inputs.make_inputs(w, seed=0)`` with the upstream gradient equal to dY on the
@@ -65,7 +66,8 @@ def sample_rows(S: int) -> np.ndarray:
     return np.array(sorted(r for r in rows if 0 <= r < S), dtype=np.int64)
 
 
-FULLSIZE = ("bf16_7b_s32768", "bf16_rl_s96000", "bf16_13b_s65536", "bf16_13b_s8192", "bf16_13b_s32768")
+FULLSIZE = ("bf16_7b_s32768", "bf16_rl_s96000", "bf16_13b_s65536", "bf16_13b_s8192", "bf16_13b_s32768",
+            "bf16_dh64_nc_s32768")
 
 
 def expected_path(name: str) -> str:

@@ -1,5 +1,6 @@
 """Full-size sampled parity: the 7B-, RL- and 13B-shaped layers at their full sequence
-lengths, and the 13B-shaped layer at S = 8192 and 32768 of its sweep, run through the
+lengths, the 13B-shaped layer at S = 8192 and 32768 of its sweep, and a 1B-width layer
+with heads of 64 and no causal mask at S = 32768, run through the
 C ABI in the launch configuration bench.py times (automatic FFN grouping; outputs
 stored in fp32 here, which changes only the final store of Y and dX), against float64
 values the rows oracle computed on the same seeded inputs (written by
