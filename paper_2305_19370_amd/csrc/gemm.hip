@@ -2,10 +2,10 @@
 //
 // Every dense contraction of the layer (QKV / output projections, both FFN
 // linears and all their weight / input gradients) is issued in this one "NT"
-// form. Operands are normally contiguous along K; a plain-store GEMM may also take
-// either operand stored K-major (token-major activations contracted over tokens,
-// feature-major gradients contracted over features), which the kernel transposes
-// on its way from LDS into the MFMA registers.
+// form. Operands are normally contiguous along K; either one may also be stored
+// K-major (weights as the caller stores them, token-major activations contracted over
+// tokens, feature-major gradients contracted over features), which the kernel
+// transposes on its way from LDS into the MFMA registers.
 //
 // bf16 path: gfx950 MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation; tiles of 256 x 256
 // with 8 waves (2 along M x 4 along N, two per SIMD) or, where fewer than 256 such tiles
