@@ -528,6 +528,15 @@ __global__ __launch_bounds__(256) void copy2d_kernel(const T* in, int64_t ld_in,
     out[r * ld_out + c] = in[r * ld_in + c];
 }
 
+// The same with 16-byte copies, for rows whose strides, width and base are multiples of 16
+// bytes.
+__global__ __launch_bounds__(256) void copy2d16_kernel(const u32x4* in, int64_t ld_in, u32x4* out, int64_t ld_out,
+                                                       int64_t cols) {   // strides and cols in 16-byte units
+  const int64_t r = blockIdx.y;
+  for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < cols; c += (int64_t)gridDim.x * 256)
+    out[r * ld_out + c] = in[r * ld_in + c];
+}
+
 // ------------------------------------------------------------------ host launchers
 
 // ------------------------------------------------------------------ cross-entropy rows
@@ -745,6 +754,15 @@ hipError_t transpose(Dt t, const void* in, int64_t ld_in, int64_t s_in, void* ou
 hipError_t copy2d(Dt t, const void* in, int64_t ld_in, void* out, int64_t ld_out, int64_t rows,
                   int64_t cols, hipStream_t s) {
   if (rows <= 0 || cols <= 0) return hipSuccess;
+  const int64_t per16 = 16 / (t == F32 ? 4 : 2);   // elements per 16 bytes
+  if (ld_in % per16 == 0 && ld_out % per16 == 0 && cols % per16 == 0 && ((uintptr_t)in & 15) == 0 &&
+      ((uintptr_t)out & 15) == 0) {
+    const int64_t c16 = cols / per16;
+    const unsigned gx = (unsigned)((c16 + 255) / 256 < 64 ? (c16 + 255) / 256 : 64);
+    hipLaunchKernelGGL(copy2d16_kernel, dim3(gx, (unsigned)rows), dim3(256), 0, s, (const u32x4*)in,
+                       ld_in / per16, (u32x4*)out, ld_out / per16, c16);
+    return hipGetLastError();
+  }
   const unsigned gx = (unsigned)((cols + 255) / 256 < 64 ? (cols + 255) / 256 : 64);
   BPT_T(t, T, hipLaunchKernelGGL((copy2d_kernel<T>), dim3(gx, (unsigned)rows), dim3(256), 0, s,
                                  (const T*)in, ld_in, (T*)out, ld_out, cols));
